@@ -1,0 +1,183 @@
+"""Reference oracle for the LRAM lattice lookup -- TEST INFRASTRUCTURE ONLY.
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg may import
+this package.  The product library never imports, links or calls it, and it
+never imports the product: the two share nothing but the seeded input
+generators in ``workloads.py``.
+
+What it computes (Goucher & Troll, "Differentiable Random Access Memory using
+Lattices"):
+
+* ``neighbors``  -- the closest 32 lattice points of Lambda = 2*E8 (Sec. 2.4)
+  within the kernel support r^2 < 8 (Sec. 2.5, Sec. 2.6), enumerated straight
+  from the definition by the C helper ``lram_oracle.c``; their locations on the
+  torus (Sec. 2.2), the fp32 recipe distances that decide the selection and
+  the kernel weights f(r) = (1 - r^2/8)^4 in fp64.
+* ``forward``    -- phi_32(q) = sum_j w_j v_{slot_j} (Sec. 2.2 with the
+  truncation of Sec. 2.6), accumulated in fp64.
+* ``backward``   -- the gradients of <G, phi_32(q)> with respect to the value
+  table (dV[s] = sum over (l,j) with slot_j(l) = s of w_j G_l) and to the query
+  (dq_i = sum_j -2 u_j^3 (x_i - k_{j,i}) <G, v_j>, u = 1 - r^2/8, the factor 2
+  being dx/dq), with the selection held fixed (Sec. 2.6: the kernel returns
+  the weights and their partial derivatives for an autograd wrapper).
+
+Scale and the other readings of the paper are stated in the header of
+``lram_oracle.c``.  All functions take numpy arrays on the host.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+NB = 32
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "lram_oracle.c")
+_BUILD = os.path.join(_HERE, "_build")
+_LIB_PATH = os.path.join(_BUILD, "liblram_oracle.so")
+_lock = threading.Lock()
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    """Compile the C helper with gcc (OpenMP, no FP contraction)."""
+    os.makedirs(_BUILD, exist_ok=True)
+    if force or not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp",
+               "-ffp-contract=off", "-fno-fast-math", _SRC, "-o", tmp, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    with _lock:
+        if _lib is None:
+            build()
+            lib = ctypes.CDLL(_LIB_PATH)
+            P = ctypes.c_void_p
+            lib.lram_oracle_neighbors.argtypes = [P, ctypes.c_int64, P, P, P, P, P, P, P, P, P, P]
+            lib.lram_oracle_neighbors.restype = ctypes.c_int
+            lib.lram_oracle_locations.argtypes = [P, ctypes.c_int64, P, P]
+            lib.lram_oracle_locations.restype = None
+            lib.lram_oracle_recipe_d2.argtypes = [P, P, ctypes.c_int64, P]
+            lib.lram_oracle_recipe_d2.restype = None
+            _lib = lib
+    return _lib
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _check_k(K) -> np.ndarray:
+    K = np.ascontiguousarray(np.asarray(K, dtype=np.int32).reshape(8))
+    if np.any(K < 2) or np.any(K % 2):
+        raise ValueError("every K_i must be even and >= 2")
+    if np.prod(K.astype(np.int64)) >= 2 ** 31:
+        raise ValueError("N = prod(K) must be below 2^31 (int32 locations)")
+    return K
+
+
+def neighbors(q: np.ndarray, K) -> dict:
+    """Closest-32 neighbour lists of queries q[..., 8] (user scale) on torus K."""
+    K = _check_k(K)
+    q = np.ascontiguousarray(np.asarray(q, dtype=np.float32))
+    lead = q.shape[:-1]
+    assert q.shape[-1] == 8
+    qf = q.reshape(-1, 8)
+    L = qf.shape[0]
+    x = np.empty((L, 8), np.float32)
+    count = np.empty(L, np.int32)
+    slot = np.empty((L, NB), np.int32)
+    d2 = np.empty((L, NB), np.float32)
+    d64 = np.empty((L, NB), np.float64)
+    w64 = np.empty((L, NB), np.float64)
+    w32 = np.empty((L, NB), np.float32)
+    lift = np.empty((L, NB, 8), np.int32)
+    wsum = np.empty(L, np.float64)
+    if L:
+        rc = _load().lram_oracle_neighbors(_ptr(qf), L, _ptr(K), _ptr(x), _ptr(count), _ptr(slot),
+                                           _ptr(d2), _ptr(d64), _ptr(w64), _ptr(w32), _ptr(lift),
+                                           _ptr(wsum))
+        if rc != 0:
+            raise RuntimeError("oracle: support larger than expected")
+    out = dict(x=x, count=count, slot=slot, d2=d2, d64=d64, w64=w64, w32=w32, lift=lift, wsum=wsum)
+    return {k: v.reshape(lead + v.shape[1:]) for k, v in out.items()}
+
+
+def locations(k: np.ndarray, K) -> np.ndarray:
+    """Location index of explicit lattice points k[..., 8] (Lambda scale)."""
+    K = _check_k(K)
+    k = np.ascontiguousarray(np.asarray(k, dtype=np.int32))
+    lead = k.shape[:-1]
+    kf = k.reshape(-1, 8)
+    out = np.empty(kf.shape[0], np.int32)
+    if kf.shape[0]:
+        _load().lram_oracle_locations(_ptr(kf), kf.shape[0], _ptr(K), _ptr(out))
+    return out.reshape(lead)
+
+
+def recipe_d2(x: np.ndarray, k: np.ndarray) -> np.ndarray:
+    """The fp32 distance recipe for explicit pairs x[...,8] (fp32), k[...,8] (int)."""
+    x = np.ascontiguousarray(np.asarray(x, dtype=np.float32))
+    k = np.ascontiguousarray(np.broadcast_to(np.asarray(k, dtype=np.int32), x.shape))
+    lead = x.shape[:-1]
+    out = np.empty(int(np.prod(lead)) if lead else 1, np.float32)
+    if out.size:
+        _load().lram_oracle_recipe_d2(_ptr(x.reshape(-1, 8)), _ptr(k.reshape(-1, 8)), out.size, _ptr(out))
+    return out.reshape(lead)
+
+
+def gather_rows(table: np.ndarray, slot: np.ndarray) -> np.ndarray:
+    """rows[..., j, :] = table[slot[..., j]] in fp64 (zero rows for slot -1)."""
+    t = np.asarray(table, dtype=np.float64)
+    s = np.asarray(slot)
+    rows = t[np.where(s >= 0, s, 0)]
+    rows[s < 0] = 0.0
+    return rows
+
+
+def forward(nb: dict, rows: np.ndarray) -> np.ndarray:
+    """phi_32 = sum_j w_j v_{slot_j}, fp64; rows[..., 32, m] are the value rows."""
+    w = nb["w64"]
+    return np.einsum("...j,...jm->...m", w, np.asarray(rows, np.float64))
+
+
+def grad_query(nb: dict, rows: np.ndarray, G: np.ndarray) -> np.ndarray:
+    """dq[..., i] = sum_j -2 u_j^3 (x_i - k_{j,i}) <G, v_j>  (user-scale q), fp64."""
+    G = np.asarray(G, np.float64)
+    gv = np.einsum("...m,...jm->...j", G, np.asarray(rows, np.float64))
+    u = 1.0 - nb["d64"] / 8.0
+    valid = nb["slot"] >= 0
+    a = np.where(valid, -2.0 * u ** 3 * gv, 0.0)
+    e = nb["x"].astype(np.float64)[..., None, :] - nb["lift"].astype(np.float64)
+    return np.einsum("...j,...ji->...i", a, e)
+
+
+def grad_table_rows(nb: dict, G: np.ndarray):
+    """Value-table gradient as (unique slots, rows): dV[s] = sum_{(l,j): slot=s} w_j G_l, fp64."""
+    G = np.asarray(G, np.float64)
+    m = G.shape[-1]
+    slot = nb["slot"].reshape(-1, NB)
+    w = nb["w64"].reshape(-1, NB)
+    Gf = G.reshape(-1, m)
+    valid = slot >= 0
+    s = slot[valid]
+    contrib = (w[:, :, None] * Gf[:, None, :])[valid]
+    uniq, inv = np.unique(s, return_inverse=True)
+    acc = np.zeros((uniq.size, m), np.float64)
+    np.add.at(acc, inv, contrib)
+    return uniq.astype(np.int64), acc
+
+
+def grad_table_dense(nb: dict, G: np.ndarray, N: int) -> np.ndarray:
+    uniq, acc = grad_table_rows(nb, G)
+    out = np.zeros((N, acc.shape[1] if acc.ndim == 2 else np.asarray(G).shape[-1]), np.float64)
+    out[uniq] = acc
+    return out
