@@ -157,6 +157,8 @@ def grad_query(nb: dict, rows: np.ndarray, G: np.ndarray) -> np.ndarray:
     valid = nb["slot"] >= 0
     a = np.where(valid, -2.0 * u ** 3 * gv, 0.0)
     e = nb["x"].astype(np.float64)[..., None, :] - nb["lift"].astype(np.float64)
+    # padded entries (and every entry of a non-finite query) contribute nothing
+    e = np.where(valid[..., None], e, 0.0)
     return np.einsum("...j,...ji->...i", a, e)
 
 
