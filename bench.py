@@ -1,0 +1,208 @@
+#!/usr/bin/env python3
+"""Benchmark of the LRAM lookup hot path on one MI355X.
+
+One step = the whole path on one batch: lram_forward (wrap, closest point,
+reduction to F, candidate scan, top-32, locations, weights, gather-reduce) then
+lram_backward (the same search, value-gradient scatter into an fp32 gradient
+table, query gradient).  Inputs are resident in HBM before timing starts; the
+gradient table accumulates across steps (it is zeroed once, outside timing).
+
+Prints one JSON line (rank 0, N = 1).  ``value`` is fwd+bwd lookups per second;
+``roofline`` covers the kernel that takes longest per step, priced with
+compulsory HBM bytes (each distinct table row counted once per launch) over its
+average launch time measured with HIP events on its own stream;
+``cpu_baseline`` times the CPU oracle on a bounded sample of the same lookups.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def pick_workload(W, name, torch):
+    w = W.WORKLOADS[name]
+    free, total = torch.cuda.mem_get_info()
+    st = 4 if w.dtype == "f32" else 2
+    need = w.table_bytes + (w.N * w.m * 4 if w.backward else 0) + w.L * (32 + w.m * 4 + w.m * st + 32) + (3 << 30)
+    log("device memory: free %.1f GB of %.1f GB; %s needs %.1f GB" % (free / 1e9, total / 1e9, name, need / 1e9))
+    return w, need <= free
+
+
+def unique_rows(lram, q, K, torch):
+    """Number of distinct table rows the batch touches (for compulsory bytes)."""
+    L = q.shape[0] * q.shape[1]
+    seen = None
+    chunk = 1 << 20
+    qf = q.reshape(-1, 8)
+    for s in range(0, L, chunk):
+        slot, _, _ = lram.neighbors(qf[s:s + chunk], K, want_d2=False)
+        u = torch.unique(slot[slot >= 0])
+        seen = u if seen is None else torch.unique(torch.cat([seen, u]))
+        del slot
+    return int(seen.numel())
+
+
+def cpu_baseline(oracle, W, w, q_np, table, G, target_s, torch):
+    """The oracle on a bounded random sample of the workload's lookups (fwd+bwd)."""
+    qf = q_np.reshape(-1, 8)
+    Gf = G.reshape(-1, w.m)
+    rng = np.random.default_rng(123)
+    n = 256
+    while True:
+        idx = np.sort(rng.choice(qf.shape[0], n, replace=False))
+        qs = qf[idx]
+        t0 = time.perf_counter()
+        nb = oracle.neighbors(qs, w.K)
+        t_nb = time.perf_counter() - t0
+        sl = torch.from_numpy(nb["slot"]).to(table.device).long()
+        rows = table[sl.clamp(min=0)].float()
+        rows[sl < 0] = 0
+        rows = rows.cpu().numpy().astype(np.float64)
+        g = Gf[torch.from_numpy(idx).to(table.device)].cpu().numpy().astype(np.float64)
+        t1 = time.perf_counter()
+        oracle.forward(nb, rows)
+        oracle.grad_query(nb, rows, g)
+        oracle.grad_table_rows(nb, g)
+        t_alg = time.perf_counter() - t1
+        t = t_nb + t_alg
+        if t >= 0.5 * target_s or n >= qf.shape[0]:
+            break
+        n = int(min(qf.shape[0], max(2 * n, n * target_s / max(t, 1e-3))))
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": n / t, "unit": "lookups/s (fwd+bwd)", "cores": cores, "kind": "oracle",
+            "sample": "%d random lookups of the %s batch (%.1f s: neighbour enumeration %.1f s in C/OpenMP, "
+                      "fp64 gather/grad algebra %.1f s in numpy; rows copied from the GPU table untimed)"
+                      % (n, w.name, t, t_nb, t_alg)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=15)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="k14-m32-bf16-zipf")
+    ap.add_argument("--mode", default="atomic", choices=["atomic", "sorted"])
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path (each GPU would run the "
+              "same kernels on its own shard of the table; see DESIGN.md). Use --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2107_03474_amd as lram
+    import workloads as W
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+    lram.load()
+    w, fits = pick_workload(W, args.workload, torch)
+    if not fits:
+        log("%s does not fit in device memory; falling back to k12-m64-bf16-proj" % w.name)
+        w, fits = pick_workload(W, "k12-m64-bf16-proj", torch)
+        if not fits:
+            raise SystemExit("no workload fits")
+    log("workload %s: %s" % (w.name, w.desc))
+    t0 = time.time()
+    q_np = W.queries(w)
+    q = torch.from_numpy(q_np).to(dev)
+    table = W.make_table(w, dev)
+    G = W.grad_out(w, dev)
+    gtab = torch.zeros((w.N, w.m), dtype=torch.float32, device=dev)
+    out = torch.empty((w.B, w.H, w.m), dtype=table.dtype, device=dev)
+    gq = torch.empty((w.B, w.H, 8), dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    log("inputs ready in %.1f s" % (time.time() - t0))
+    U = unique_rows(lram, q, w.K, torch)
+    log("distinct rows touched: %d of %d slots (%.1f%%)" % (U, w.L * 32, 100.0 * U / (w.L * 32)))
+
+    stream = torch.cuda.current_stream()
+
+    def step():
+        lram.forward(q, table, w.K, out=out)
+        lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, mode=args.mode)
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        log("warmup %d done" % i)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(args.steps):
+        ev[k][0].record(stream)
+        lram.forward(q, table, w.K, out=out)
+        ev[k][1].record(stream)
+        lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, mode=args.mode)
+        ev[k][2].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    fwd_ms = float(np.mean([ev[k][0].elapsed_time(ev[k][1]) for k in range(args.steps)]))
+    bwd_ms = float(np.mean([ev[k][1].elapsed_time(ev[k][2]) for k in range(args.steps)]))
+    ms_step = wall * 1e3 / args.steps
+    log("timed %d steps: %.3f ms/step (forward %.3f ms, backward %.3f ms)" % (args.steps, ms_step, fwd_ms, bwd_ms))
+
+    st = 4 if w.dtype == "f32" else 2
+    L = w.L
+    fwd_bytes = L * (32 + w.m * st) + U * w.m * st
+    bwd_bytes = L * (32 + w.m * 4 + 32) + U * (w.m * st + 2 * w.m * 4)
+    fwd_req = L * (32 + w.m * st + 32 * w.m * st)
+    bwd_req = L * (32 + w.m * 4 + 32 + 32 * (w.m * st + 2 * w.m * 4))
+    if bwd_ms >= fwd_ms:
+        kname, kms, kbytes, kreq = "k_backward_atomic", bwd_ms, bwd_bytes, bwd_req
+    else:
+        kname, kms, kbytes, kreq = "k_forward", fwd_ms, fwd_bytes, fwd_req
+    achieved = kbytes / (kms * 1e-3) / 1e9
+    res = {
+        "metric": "lookups/sec fwd and fwd+bwd; achieved HBM GB/s vs peak (1 GPU)",
+        "value": L / (ms_step * 1e-3),
+        "unit": "lookups/s (fwd+bwd)",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 table, fp32 accumulate" if w.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded; see workloads.py)",
+        "config": {"workload": w.name, "K": list(w.K), "locations": w.N, "m": w.m, "table_dtype": w.dtype,
+                   "batch": w.B, "heads": w.H, "lookups": L, "scatter": args.mode, "parallelism": "none (1 GPU)"},
+        "fwd_lookups_per_s": L / (fwd_ms * 1e-3),
+        "fwd_ms": fwd_ms,
+        "bwd_ms": bwd_ms,
+        "distinct_rows": U,
+        "roofline": {"kernel": kname, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "bytes_per_launch": kbytes, "requested_bytes_per_launch": kreq,
+                     "requested_GBps": kreq / (kms * 1e-3) / 1e9},
+        "fwd_hbm_GBps": fwd_bytes / (fwd_ms * 1e-3) / 1e9,
+        "bwd_hbm_GBps": bwd_bytes / (bwd_ms * 1e-3) / 1e9,
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+
+        log("cpu baseline (oracle) ...")
+        res["cpu_baseline"] = cpu_baseline(oracle, W, w, q_np, table, G, args.cpu_seconds, torch)
+        log("cpu baseline done")
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

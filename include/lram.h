@@ -1,0 +1,132 @@
+/*
+ * lram.h -- C ABI of liblram.so, the LRAM lattice lookup on AMD Instinct MI355X (gfx950).
+ *
+ * Goucher & Troll, "Differentiable Random Access Memory using Lattices":
+ * a memory of N = prod K_i value vectors v_s in R^m stored at the locations of
+ * the lattice Lambda = 2*E8 (Sec. 2.4) on the torus T_K (Sec. 2.2).  A lookup
+ * maps a query q in R^8 to
+ *
+ *     phi(q) = sum_{j < 32} f(|x - k_j|) v_{slot(k_j)},   f(r) = max(0, 1 - r^2/8)^4,
+ *
+ * over the 32 lattice points k_j closest to x (Sec. 2.5 kernel, Sec. 2.6
+ * truncation to k = 32, no renormalisation).
+ *
+ * Conventions shared by every entry point:
+ *   - Scale.  q is given at the unimodular-E8 scale on a torus of side K_i, so
+ *     q_i in [0, K_i) covers it once; the lattice work happens at the doubled
+ *     scale of Sec. 2.4, x_i = fmodf(2 q_i, 2 K_i) (exact; a negative q_i keeps
+ *     its sign; any real q_i is accepted).
+ *   - K.  Eight even integers K_i >= 2 (host array); N = prod K_i < 2^31.
+ *   - Locations.  slot(k) = eps*N/2 + ((..(Y_0 K_1 + Y_1) K_2 + ..) K_6 + Y_6)*(K_7/2)
+ *     + floor(Y_7/2), with eps = k_0 mod 2 and Y_i = ((k_i - eps)/2) mod K_i:
+ *     row slot of the value table holds v at that location (Sec. 2.2, M = Lambda/L_K).
+ *   - Selection.  The squared distance that decides the 32 is the fp32 recipe
+ *     e_i = fl(x_i - k_i), s = e_0^2, s = fl(s + fl(e_i^2)) for i = 1..7, no
+ *     FMA; support is s < 8 (open ball, Sec. 2.5); order is ascending
+ *     (bits of s, slot, k lexicographic).  Fewer than 32 points in the support
+ *     (only at exceptional queries such as lattice points or deep holes) are
+ *     padded with slot -1 and weight 0.  A non-finite query coordinate gives an
+ *     all-padding list.
+ *   - Layout.  Every tensor is dense row-major: q [L][8] fp32, table [N][m],
+ *     out [L][m] (table dtype), grad_out [L][m] fp32, grad_table [N][m] fp32,
+ *     grad_q [L][8] fp32, with L = B*H lookups (heads share the table,
+ *     Sec. 2.3).  Device pointers must be 16-byte aligned.
+ *   - dtype/m.  LRAM_F32 or LRAM_BF16 tables with m in {32, 64}; accumulation is
+ *     always fp32.
+ *   - Streams.  stream is a hipStream_t (NULL = the null stream).  All work is
+ *     enqueued asynchronously; nothing synchronises.  Arguments are checked on
+ *     the host before anything is launched; a failed check launches nothing.
+ *   - Memory.  The caller owns every buffer.  The library allocates no device
+ *     memory and keeps no mutable global state: calls on different streams
+ *     may overlap (but see lram_backward on grad_table).
+ *   - Errors.  Return value LRAM_OK (0) or one of lram_status below.  Faults of
+ *     the asynchronous kernels surface at the caller's next synchronisation.
+ */
+#ifndef LRAM_H
+#define LRAM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LRAM_NEIGHBOURS 32
+
+typedef enum {
+  LRAM_OK = 0,
+  LRAM_EINVAL = 1,      /* null pointer with L > 0, negative size, misaligned pointer */
+  LRAM_EBADK = 2,       /* a K_i odd or < 2, N != prod K, or N >= 2^31 */
+  LRAM_EDTYPE = 3,      /* unknown dtype or unsupported m for that dtype */
+  LRAM_EWORKSPACE = 4,  /* workspace missing or smaller than lram_backward_workspace_bytes */
+  LRAM_EMODE = 5,       /* unknown scatter mode */
+  LRAM_EHIP = 6         /* a HIP launch failed; see lram_last_hip_error */
+} lram_status;
+
+typedef enum { LRAM_F32 = 0, LRAM_BF16 = 1 } lram_dtype;
+
+typedef enum {
+  LRAM_SCATTER_ATOMIC = 0, /* fp32 atomic adds straight into grad_table */
+  LRAM_SCATTER_SORTED = 1  /* sort (slot, lookup) pairs, one read-modify-write per touched row */
+} lram_scatter_mode;
+
+/* Library version (major*10000 + minor*100 + patch). */
+int lram_version(void);
+
+/* Static description of a status code. */
+const char* lram_strerror(int status);
+
+/* hipError_t of the most recent LRAM_EHIP on the calling thread (0 if none). */
+int lram_last_hip_error(void);
+
+/*
+ * lram_neighbors -- the neighbour lists themselves (Sec. 2.6: the kernel's
+ * indices alpha_i and weights w_i).  For each of L = B*H lookups writes, in
+ * selection order:
+ *   slot [L][32] int32  locations, -1 for padding
+ *   w    [L][32] fp32   fp32 recipe weight u = fl(1 - s*0.125f), w = fl(fl(u*u)*fl(u*u)); 0 for padding
+ *   d2   [L][32] fp32   recipe squared distance s (nullable); +inf for padding
+ * Device pointers.  B, H >= 0; B*H == 0 is a no-op.
+ */
+int lram_neighbors(const float* q, int64_t B, int64_t H, const int32_t K[8], int32_t* slot, float* w,
+                   float* d2, void* stream);
+
+/*
+ * lram_forward -- out[l][:] = sum_j w_j table[slot_j][:] (Sec. 2.2 with the
+ * truncation of Sec. 2.6), fp32 accumulation, written once in the table dtype
+ * (bf16: round to nearest even).  table holds N rows of m elements.
+ */
+int lram_forward(const float* q, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
+                 int64_t N, int32_t m, void* out, void* stream);
+
+/*
+ * lram_backward_workspace_bytes -- device workspace needed by lram_backward
+ * for L = B*H lookups in the given scatter mode (0 for LRAM_SCATTER_ATOMIC).
+ */
+int lram_backward_workspace_bytes(int64_t B, int64_t H, int32_t m, int mode, size_t* bytes);
+
+/*
+ * lram_backward -- gradients of sum_l <grad_out[l], phi(q_l)> with the selection
+ * held fixed (Sec. 2.6: the kernel supplies the weights and their derivatives
+ * to an autograd wrapper):
+ *   grad_table[s][:] += sum over (l, j) with slot_j(l) = s of w_j grad_out[l][:]
+ *       (accumulated: the caller zeroes grad_table once; untouched rows are not
+ *        written; concurrent calls on other streams that update the same
+ *        grad_table race only in rounding order under LRAM_SCATTER_ATOMIC and
+ *        must not overlap under LRAM_SCATTER_SORTED)
+ *   grad_q[l][i] = sum_j -2 u_j^3 (x_i - k_{j,i}) <grad_out[l], table[slot_j]>,
+ *       u_j = 1 - s_j/8 (overwritten; nullable to skip it)
+ * The neighbour search is recomputed from q.  workspace/ws_bytes: device
+ * buffer of at least lram_backward_workspace_bytes (may be NULL for the atomic
+ * mode).  grad_table may be NULL only if grad_q is not.
+ */
+int lram_backward(const float* q, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
+                  int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_q, int mode,
+                  void* workspace, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LRAM_H */

@@ -1,0 +1,195 @@
+"""LRAM lattice lookup on AMD Instinct MI355X -- Python binding of liblram.so.
+
+Goucher & Troll, "Differentiable Random Access Memory using Lattices": the
+lookup phi of Sec. 2.2 over Lambda = 2*E8 (Sec. 2.4) with the kernel of Sec. 2.5,
+truncated to the closest 32 points found by the symmetry reduction of Sec. 2.6,
+and its backward.
+
+This module only marshals torch tensors (device memory) and the current HIP
+stream into the C ABI declared in ``include/lram.h``; every step of the lookup
+runs in the library's HIP kernels.  There is no fallback: if the library is not
+built, or a call is made without a GPU, it raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+from typing import Optional, Sequence, Tuple
+
+import torch  # noqa: F401  -- loads the HIP runtime liblram.so must share
+
+__all__ = ["neighbors", "forward", "backward", "backward_workspace_bytes", "lookup", "LramLookup",
+           "library_path", "load", "LramError", "F32", "BF16", "SCATTER_ATOMIC", "SCATTER_SORTED", "NB"]
+
+NB = 32
+F32, BF16 = 0, 1
+SCATTER_ATOMIC, SCATTER_SORTED = 0, 1
+_MODES = {"atomic": SCATTER_ATOMIC, "sorted": SCATTER_SORTED, SCATTER_ATOMIC: SCATTER_ATOMIC,
+          SCATTER_SORTED: SCATTER_SORTED}
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "_build", "liblram.so")
+_lock = threading.Lock()
+_lib = None
+
+
+class LramError(RuntimeError):
+    pass
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def load():
+    """Load liblram.so (built in-tree by ``paper_2107_03474_amd.build``)."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(_LIB_PATH):
+                raise LramError("liblram.so is not built (%s); run paper_2107_03474_amd/build.py" % _LIB_PATH)
+            lib = ctypes.CDLL(_LIB_PATH)
+            P, I64, I32, I = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int
+            lib.lram_version.restype = I
+            lib.lram_strerror.argtypes = [I]
+            lib.lram_strerror.restype = ctypes.c_char_p
+            lib.lram_last_hip_error.restype = I
+            lib.lram_neighbors.argtypes = [P, I64, I64, P, P, P, P, P]
+            lib.lram_neighbors.restype = I
+            lib.lram_forward.argtypes = [P, I64, I64, P, P, I, I64, I32, P, P]
+            lib.lram_forward.restype = I
+            lib.lram_backward_workspace_bytes.argtypes = [I64, I64, I32, I, ctypes.POINTER(ctypes.c_size_t)]
+            lib.lram_backward_workspace_bytes.restype = I
+            lib.lram_backward.argtypes = [P, I64, I64, P, P, I, I64, I32, P, P, P, I, P, ctypes.c_size_t, P]
+            lib.lram_backward.restype = I
+            _lib = lib
+    return _lib
+
+
+def _check(rc: int):
+    if rc != 0:
+        lib = load()
+        msg = lib.lram_strerror(rc).decode()
+        if rc == 6:
+            msg += " (hipError %d)" % lib.lram_last_hip_error()
+        raise LramError(msg)
+
+
+def _K(K: Sequence[int]):
+    k = [int(v) for v in K]
+    if len(k) != 8:
+        raise LramError("K must have 8 entries")
+    return (ctypes.c_int32 * 8)(*k)
+
+
+def _stream(t: torch.Tensor):
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _dev(t: torch.Tensor, name: str, dtype=None):
+    if not t.is_cuda:
+        raise LramError("%s must be a GPU tensor" % name)
+    if not t.is_contiguous():
+        raise LramError("%s must be contiguous" % name)
+    if dtype is not None and t.dtype != dtype:
+        raise LramError("%s must be %s" % (name, dtype))
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _table_dtype(table: torch.Tensor) -> int:
+    if table.dtype == torch.float32:
+        return F32
+    if table.dtype == torch.bfloat16:
+        return BF16
+    raise LramError("table must be float32 or bfloat16")
+
+
+def _bh(q: torch.Tensor) -> Tuple[int, int]:
+    if q.dim() == 2:
+        return q.shape[0], 1
+    if q.dim() == 3:
+        return q.shape[0], q.shape[1]
+    raise LramError("q must be [B, H, 8] or [L, 8]")
+
+
+def neighbors(q: torch.Tensor, K: Sequence[int], want_d2: bool = True):
+    """Neighbour lists: (slot int32, w fp32, d2 fp32 or None), each [..., 32]."""
+    lib = load()
+    B, H = _bh(q)
+    lead = q.shape[:-1]
+    slot = torch.empty(lead + (NB,), dtype=torch.int32, device=q.device)
+    w = torch.empty(lead + (NB,), dtype=torch.float32, device=q.device)
+    d2 = torch.empty(lead + (NB,), dtype=torch.float32, device=q.device) if want_d2 else None
+    _check(lib.lram_neighbors(_dev(q, "q", torch.float32), B, H, _K(K), _dev(slot, "slot"), _dev(w, "w"),
+                              _dev(d2, "d2") if d2 is not None else None, _stream(q)))
+    return slot, w, d2
+
+
+def forward(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], out: Optional[torch.Tensor] = None):
+    """phi(q): [..., m] in the table dtype."""
+    lib = load()
+    B, H = _bh(q)
+    N, m = table.shape
+    if out is None:
+        out = torch.empty(q.shape[:-1] + (m,), dtype=table.dtype, device=q.device)
+    _check(lib.lram_forward(_dev(q, "q", torch.float32), B, H, _K(K), _dev(table, "table"), _table_dtype(table),
+                            N, m, _dev(out, "out", table.dtype), _stream(q)))
+    return out
+
+
+def backward_workspace_bytes(B: int, H: int, m: int, mode="atomic") -> int:
+    lib = load()
+    n = ctypes.c_size_t(0)
+    _check(lib.lram_backward_workspace_bytes(B, H, m, _MODES[mode], ctypes.byref(n)))
+    return n.value
+
+
+def backward(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], grad_out: torch.Tensor,
+             grad_table: Optional[torch.Tensor] = None, want_grad_q: bool = True, mode="atomic",
+             workspace: Optional[torch.Tensor] = None, grad_q: Optional[torch.Tensor] = None):
+    """Gradients: grad_table [N, m] fp32 is ACCUMULATED into (allocated zeroed if None,
+    pass False to skip), grad_q [..., 8] fp32 (None unless want_grad_q; written into
+    ``grad_q`` when given)."""
+    lib = load()
+    B, H = _bh(q)
+    N, m = table.shape
+    if grad_table is None:
+        grad_table = torch.zeros((N, m), dtype=torch.float32, device=q.device)
+    gq = None
+    if want_grad_q:
+        gq = grad_q if grad_q is not None else torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    mode_i = _MODES[mode]
+    ws_bytes = backward_workspace_bytes(B, H, m, mode_i)
+    if ws_bytes and workspace is None:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
+    gt_ptr = _dev(grad_table, "grad_table", torch.float32) if grad_table is not False else None
+    _check(lib.lram_backward(_dev(q, "q", torch.float32), B, H, _K(K), _dev(table, "table"), _table_dtype(table),
+                             N, m, _dev(grad_out, "grad_out", torch.float32), gt_ptr,
+                             _dev(gq, "grad_q") if gq is not None else None, mode_i,
+                             _dev(workspace, "workspace") if workspace is not None else None,
+                             workspace.numel() if workspace is not None else 0, _stream(q)))
+    return (grad_table if grad_table is not False else None), gq
+
+
+class LramLookup(torch.autograd.Function):
+    """Autograd wrapper (Sec. 2.6): forward phi(q); backward gives dq and a dense dtable."""
+
+    @staticmethod
+    def forward(ctx, q, table, K, mode):
+        ctx.save_for_backward(q, table)
+        ctx.K = tuple(int(k) for k in K)
+        ctx.mode = mode
+        return forward(q.contiguous(), table.contiguous(), ctx.K)
+
+    @staticmethod
+    def backward(ctx, g):
+        q, table = ctx.saved_tensors
+        g32 = g.contiguous().to(torch.float32)
+        gt, gq = backward(q, table, ctx.K, g32, grad_table=None if ctx.needs_input_grad[1] else False,
+                          want_grad_q=ctx.needs_input_grad[0], mode=ctx.mode)
+        return gq, (gt.to(table.dtype) if gt is not None else None), None, None
+
+
+def lookup(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], mode="atomic") -> torch.Tensor:
+    return LramLookup.apply(q, table, tuple(K), mode)

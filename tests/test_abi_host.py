@@ -1,0 +1,102 @@
+"""Host-side checks of the C ABI: the library loads, exports every entry point
+declared in include/lram.h, and rejects bad arguments before launching anything.
+No GPU is needed: every call here fails (or returns) in host validation."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2107_03474_amd as lram
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lram.h")
+
+
+def _declared():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(lram_[a-z_0-9]+)\s*\(", txt)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return lram.load()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = _declared()
+    assert {"lram_forward", "lram_backward", "lram_neighbors", "lram_backward_workspace_bytes",
+            "lram_strerror", "lram_version", "lram_last_hip_error"} <= set(names)
+    out = subprocess.run(["nm", "-D", "--defined-only", lram.library_path()], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(re.findall(r"\bT (lram_[a-z_0-9]+)", out))
+    assert set(names) <= exported, set(names) - exported
+    for n in names:
+        assert hasattr(lib, n)
+
+
+def test_version_and_strerror(lib):
+    assert lib.lram_version() >= 100
+    for rc in range(7):
+        assert len(lib.lram_strerror(rc)) > 0
+    assert b"unknown" in lib.lram_strerror(99)
+
+
+K4 = (ctypes.c_int32 * 8)(*([4] * 8))
+FAKE = ctypes.c_void_p(0x10000)      # never dereferenced: validation fails first
+FAKE_MIS = ctypes.c_void_p(0x10004)  # misaligned
+
+
+def _fwd(lib, q=FAKE, B=4, H=1, K=K4, table=FAKE, dtype=0, N=4 ** 8, m=32, out=FAKE):
+    return lib.lram_forward(q, B, H, K, table, dtype, N, m, out, None)
+
+
+def test_forward_validation(lib):
+    assert _fwd(lib, K=(ctypes.c_int32 * 8)(*([3] + [4] * 7))) == 2          # odd K
+    assert _fwd(lib, K=(ctypes.c_int32 * 8)(*([0] + [4] * 7))) == 2          # K < 2
+    assert _fwd(lib, K=(ctypes.c_int32 * 8)(*([16] * 8))) == 2                # N >= 2^31
+    assert _fwd(lib, N=12345) == 2                                            # N != prod K
+    assert _fwd(lib, dtype=7) == 3
+    assert _fwd(lib, m=48) == 3
+    assert _fwd(lib, q=None) == 1
+    assert _fwd(lib, q=FAKE_MIS) == 1
+    assert _fwd(lib, table=None) == 1
+    assert _fwd(lib, out=None) == 1
+    assert _fwd(lib, B=-1) == 1
+    assert _fwd(lib, q=None, table=None, out=None, B=0) == 0                  # empty: no-op
+    assert _fwd(lib, q=None, table=None, out=None, H=0) == 0
+
+
+def test_neighbors_validation(lib):
+    assert lib.lram_neighbors(FAKE, 4, 1, (ctypes.c_int32 * 8)(*([5] * 8)), FAKE, FAKE, None, None) == 2
+    assert lib.lram_neighbors(FAKE, 4, 1, K4, None, FAKE, None, None) == 1
+    assert lib.lram_neighbors(None, 0, 7, K4, None, None, None, None) == 0
+
+
+def test_backward_validation(lib):
+    def bwd(grad_out=FAKE, gt=FAKE, gq=FAKE, mode=0, K=K4, B=4, ws=None, wsb=0):
+        return lib.lram_backward(FAKE, B, 1, K, FAKE, 0, 4 ** 8, 32, grad_out, gt, gq, mode, ws, wsb, None)
+
+    assert bwd(mode=9) == 5
+    assert bwd(grad_out=None) == 1
+    assert bwd(gt=None, gq=None) == 1
+    assert bwd(K=(ctypes.c_int32 * 8)(*([4] * 7 + [7]))) == 2
+    assert bwd(B=0, grad_out=None) == 0
+    n = ctypes.c_size_t(123)
+    assert lib.lram_backward_workspace_bytes(4, 1, 32, 0, ctypes.byref(n)) == 0 and n.value == 0
+    assert lib.lram_backward_workspace_bytes(4, 1, 32, 9, ctypes.byref(n)) == 5
+    assert lib.lram_backward_workspace_bytes(4, 1, 48, 0, ctypes.byref(n)) == 3
+
+
+def test_no_oracle_in_product():
+    """The product package never imports or links the oracle."""
+    pkg = os.path.join(ROOT, "paper_2107_03474_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".cpp", ".h", ".inc")):
+                txt = open(os.path.join(dirpath, f), errors="ignore").read()
+                assert "oracle" not in txt.lower(), f
+    out = subprocess.run(["ldd", lram.library_path()], capture_output=True, text=True).stdout
+    assert "oracle" not in out

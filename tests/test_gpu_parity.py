@@ -1,0 +1,211 @@
+"""GPU parity: the HIP library (through the C ABI) against the oracle.
+
+Bars (fixed before any kernel ran):
+  * neighbour locations: bit-exact, in selection order; recipe distances and
+    recipe weights: bit-exact (they are decided in the same fp32 arithmetic);
+  * forward and both gradients, per output row: relative L2 error <= 1e-5 for
+    fp32 tables and <= 2e-2 for bf16 tables, against the fp64 oracle;
+  * value-gradient rows no lookup touched stay exactly 0.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2107_03474_amd as lram
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+def _rel_rows(a, b):
+    """Per-row relative L2 error of a against reference b (rows with |b| = 0 use |a|)."""
+    a = np.asarray(a, np.float64).reshape(a.shape[0], -1)
+    b = np.asarray(b, np.float64).reshape(b.shape[0], -1)
+    num = np.linalg.norm(a - b, axis=1)
+    den = np.linalg.norm(b, axis=1)
+    return np.where(den > 0, num / np.where(den > 0, den, 1), num)
+
+
+def check_neighbors(q_np, K):
+    q = torch.from_numpy(np.ascontiguousarray(q_np)).to(DEV)
+    slot, w, d2 = lram.neighbors(q, K)
+    torch.cuda.synchronize()
+    nb = oracle.neighbors(q_np, K)
+    s = slot.cpu().numpy().reshape(nb["slot"].shape)
+    bad = np.nonzero((s != nb["slot"]).any(-1).reshape(-1))[0]
+    assert bad.size == 0, "first mismatching lookup %d: gpu %s oracle %s" % (
+        bad[0], s.reshape(-1, 32)[bad[0]], nb["slot"].reshape(-1, 32)[bad[0]])
+    np.testing.assert_array_equal(d2.cpu().numpy().reshape(nb["d2"].shape).view(np.uint32), nb["d2"].view(np.uint32))
+    np.testing.assert_array_equal(w.cpu().numpy().reshape(nb["w32"].shape).view(np.uint32), nb["w32"].view(np.uint32))
+    return nb
+
+
+def special_queries(K):
+    Kf = np.asarray(K, np.float64)
+    rho = np.array([0, 1, 2, 3, 4, 5, 6, 23], np.float64)
+    pts = [np.zeros(8), np.full(8, 0.5), [1, 0, 0, 0, 0, 0, 0, 0], [0.5] * 7 + [-0.5], 2.0 ** -11 * rho,
+           np.full(8, 0.5) + 2.0 ** -11 * rho, [1, 1, 0, 0, 0, 0, 0, 0.0], [0.25, 0.25, 0.25, 0.25, 0, 0, 0, 0],
+           [0.5, 0.5, 0.5, 0.5, 0.5, 0.5, 0.5, 1.0], [3, 1, 2, 0.5, 0.25, 0.125, 1.5, 2.5],
+           -np.array([1.25, 0.5, 3.0, 0.75, 2.0, 1.0, 0.5, 0.25])]
+    q = np.array(pts, np.float64)
+    q = np.concatenate([q, q + Kf * 3, q - Kf])          # the same points seen through the wrap
+    return q.astype(np.float32)
+
+
+@pytest.mark.parametrize("K", [(4,) * 8, (8,) * 8, (12,) * 8, (14,) * 8, (2, 4, 6, 8, 10, 2, 4, 6), (2,) * 8])
+def test_neighbors_random(K):
+    _say("neighbors random K=%s" % (K,))
+    rng = np.random.default_rng(7)
+    q = (rng.random((2000, 8)) * np.asarray(K)).astype(np.float32)
+    q[:200] = q[:200] * 5 - 2 * np.asarray(K, np.float32)   # out of range, negative
+    check_neighbors(q, K)
+
+
+@pytest.mark.parametrize("K", [(4,) * 8, (8,) * 8, (2, 2, 2, 2, 4, 4, 4, 4)])
+def test_neighbors_special_points(K):
+    _say("neighbors special K=%s" % (K,))
+    nb = check_neighbors(special_queries(K), K)
+    assert (nb["count"] < 32).any()
+
+
+def test_neighbors_dyadic_grid():
+    """Coarse dyadic queries produce many exact distance ties at the 32nd place."""
+    _say("neighbors dyadic")
+    rng = np.random.default_rng(8)
+    K = (8,) * 8
+    q = (rng.integers(0, 8 * 8, size=(3000, 8)) / 8.0).astype(np.float32)
+    check_neighbors(q, K)
+
+
+def test_neighbors_nonfinite_and_ragged():
+    _say("neighbors nonfinite/ragged")
+    K = (4,) * 8
+    rng = np.random.default_rng(9)
+    for L in (1, 2, 63, 64, 65, 255, 257, 1000):
+        q = (rng.random((L, 8)) * 4).astype(np.float32)
+        if L > 3:
+            q[1, 3] = np.nan
+            q[2, 0] = np.inf
+            q[3, 7] = 3e38   # 2q overflows to inf
+        nb = check_neighbors(q, K)
+        if L > 3:
+            assert np.all(nb["slot"][1:4] == -1)
+
+
+def test_neighbors_workload_queries():
+    for name in ("k4-m32-f32-uniform", "k4-m32-f32-gmm64"):
+        w = W.WORKLOADS[name]
+        _say("neighbors workload", name)
+        check_neighbors(W.queries(w).reshape(-1, 8), w.K)
+    for name in ("k8-m64-f32-uniform", "k12-m64-bf16-proj", "k14-m32-bf16-zipf"):
+        w = W.WORKLOADS[name]
+        _say("neighbors workload sample", name)
+        q = W.queries(w).reshape(-1, 8)
+        idx = np.random.default_rng(1).choice(q.shape[0], 6000, replace=False)
+        check_neighbors(q[idx], w.K)
+
+
+def test_empty_batch_is_noop():
+    q = torch.empty((0, 4, 8), dtype=torch.float32, device=DEV)
+    slot, w, d2 = lram.neighbors(q, (4,) * 8)
+    table = torch.zeros((4 ** 8, 32), device=DEV)
+    out = lram.forward(q, table, (4,) * 8)
+    assert out.shape == (0, 4, 32)
+    g = torch.empty((0, 4, 32), device=DEV)
+    gt, gq = lram.backward(q, table, (4,) * 8, g)
+    torch.cuda.synchronize()
+    assert gt.abs().sum().item() == 0
+
+
+def _small_table(K, m, dtype, seed=0):
+    N = int(np.prod(K))
+    g = torch.Generator(device=DEV)
+    g.manual_seed(seed)
+    t = torch.randn((N, m), generator=g, device=DEV) * 0.02
+    return t.to(dtype)
+
+
+def _tol(dtype):
+    return 1e-5 if dtype == torch.float32 else 2e-2
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("m", [32, 64])
+@pytest.mark.parametrize("K", [(4,) * 8, (2, 4, 6, 8, 2, 4, 6, 8)])
+def test_forward_backward_small(K, m, dtype):
+    _say("fwd/bwd K=%s m=%d %s" % (K, m, dtype))
+    rng = np.random.default_rng(11)
+    L = 3000
+    q_np = (rng.random((L, 8)) * np.asarray(K)).astype(np.float32)
+    q_np[:10] = special_queries(K)[:10]
+    q_np[10, 2] = np.nan
+    q = torch.from_numpy(q_np).to(DEV)
+    table = _small_table(K, m, dtype)
+    G = torch.randn((L, m), device=DEV, dtype=torch.float32)
+    out = lram.forward(q, table, K)
+    gt, gq = lram.backward(q, table, K, G)
+    torch.cuda.synchronize()
+    nb = oracle.neighbors(q_np, K)
+    tab = table.float().cpu().numpy()
+    rows = oracle.gather_rows(tab, nb["slot"])
+    ref = oracle.forward(nb, rows)
+    err = _rel_rows(out.float().cpu().numpy(), ref)
+    assert err.max() <= _tol(dtype), err.max()
+    # dq: the fp32 kernel vs fp64 oracle
+    Gn = G.cpu().numpy()
+    dq_ref = oracle.grad_query(nb, rows, Gn)
+    err = _rel_rows(gq.cpu().numpy(), dq_ref)
+    assert err.max() <= (1e-4 if dtype == torch.float32 else 2e-2), err.max()
+    dV_ref = oracle.grad_table_dense(nb, Gn, int(np.prod(K)))
+    dV = gt.cpu().numpy()
+    touched = np.unique(nb["slot"][nb["slot"] >= 0])
+    err = _rel_rows(dV[touched], dV_ref[touched])
+    assert err.max() <= 1e-5, err.max()
+    untouched = np.setdiff1d(np.arange(dV.shape[0]), touched)
+    assert np.all(dV[untouched] == 0)
+    assert np.all(out.float().cpu().numpy()[10] == 0) and np.all(gq.cpu().numpy()[10] == 0)
+
+
+def test_backward_accumulates():
+    K = (4,) * 8
+    rng = np.random.default_rng(12)
+    q = torch.from_numpy((rng.random((500, 8)) * 4).astype(np.float32)).to(DEV)
+    table = _small_table(K, 32, torch.float32)
+    G = torch.randn((500, 32), device=DEV)
+    gt1, _ = lram.backward(q, table, K, G)
+    gt2 = gt1.clone()
+    lram.backward(q, table, K, G, grad_table=gt2, want_grad_q=False)
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(gt2.cpu().numpy(), 2 * gt1.cpu().numpy(), rtol=1e-6, atol=1e-9)
+
+
+@pytest.mark.parametrize("name", ["k4-m32-f32-uniform", "k4-m32-f32-gmm64"])
+def test_workload_full_parity(name):
+    """Small workloads in full: every lookup, every output."""
+    w = W.WORKLOADS[name]
+    _say("full parity", name)
+    q_np = W.queries(w)
+    q = torch.from_numpy(q_np).to(DEV)
+    table = W.make_table(w, DEV)
+    G = W.grad_out(w, DEV)
+    out = lram.forward(q, table, w.K)
+    gt, gq = lram.backward(q, table, w.K, G)
+    torch.cuda.synchronize()
+    nb = oracle.neighbors(q_np, w.K)
+    rows = oracle.gather_rows(table.float().cpu().numpy(), nb["slot"])
+    assert _rel_rows(out.cpu().numpy().reshape(w.L, -1), oracle.forward(nb, rows).reshape(w.L, -1)).max() <= 1e-5
+    Gn = G.cpu().numpy()
+    dq_ref = oracle.grad_query(nb, rows, Gn)
+    assert _rel_rows(gq.cpu().numpy().reshape(w.L, -1), dq_ref.reshape(w.L, -1)).max() <= 1e-4
+    uniq, acc = oracle.grad_table_rows(nb, Gn)
+    dV = gt.cpu().numpy()
+    assert _rel_rows(dV[uniq], acc).max() <= 1e-5
+    mask = np.ones(w.N, bool)
+    mask[uniq] = False
+    assert np.all(dV[mask] == 0)

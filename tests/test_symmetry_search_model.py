@@ -1,0 +1,158 @@
+"""CPU model of the GPU neighbour search, checked against the oracle.
+
+The GPU kernels do not enumerate lattice points; they follow Sec. 2.6: find the
+closest lattice point c, carry x - c into the fundamental region F by a signed
+permutation (even number of sign changes), scan the fixed candidate list of
+points near F (``csrc/e8_candidates.inc``) mapped back by the inverse isometry,
+and keep the closest 32.  This numpy model of that design (written for the
+tests, sharing no code with the kernels) must reproduce the oracle's lists
+exactly; it validates the candidate table and the reduction on the CPU.
+"""
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+INC = os.path.join(ROOT, "paper_2107_03474_amd", "csrc", "e8_candidates.inc")
+
+
+def _read_lists():
+    txt = open(INC).read()
+    out = {}
+    for name in ("E8_STRICT_INIT", "E8_BOUNDARY_INIT"):
+        body = txt[txt.index("#define " + name):]
+        body = body[: body.index("}\n") + 1]
+        rows = re.findall(r"\{([-\d,\s]+)\}", body)
+        out[name] = np.array([[int(v) for v in r.split(",")] for r in rows], np.int64)
+    return out["E8_STRICT_INIT"], out["E8_BOUNDARY_INIT"]
+
+
+STRICT, BOUNDARY = _read_lists()
+
+
+def _d8_round(y):
+    r = np.rint(y)
+    bad = (r.sum(1) % 2) != 0
+    worst = np.argmax(np.abs(y - r), axis=1)
+    idx = np.arange(y.shape[0])
+    step = np.where(y[idx, worst] > r[idx, worst], 1.0, -1.0)
+    r[idx[bad], worst[bad]] += step[bad]
+    return r
+
+
+def _reduce(x):
+    """closest point c, F-position r_i of each coordinate and sign s'_i."""
+    c0 = 2 * _d8_round(x * np.float32(0.5))
+    c1 = 2 * _d8_round((x - np.float32(1)) * np.float32(0.5)) + 1
+    d0 = ((x - c0) ** 2).sum(1)
+    d1 = ((x - c1) ** 2).sum(1)
+    c = np.where((d1 < d0)[:, None], c1, c0).astype(np.int64)
+    y = x - c.astype(np.float32)
+    a = np.abs(y)
+    n = x.shape[0]
+    r = np.zeros((n, 8), np.int64)
+    for i in range(8):
+        for j in range(8):
+            if j != i:
+                r[:, i] += (a[:, j] > a[:, i]) | ((a[:, j] == a[:, i]) & (j < i))
+    neg = y < 0
+    odd = neg.sum(1) % 2 == 1
+    last = r == 7
+    neg = np.where(odd[:, None] & last, ~neg, neg)
+    s = np.where(neg, -1, 1)
+    return c, r, s
+
+
+def _recipe(x, k):
+    e = x[:, None, :] - k.astype(np.float32)
+    sq = e * e
+    d = sq[..., 0].copy()
+    for i in range(1, 8):
+        d = d + sq[..., i]
+    return d
+
+
+def model_neighbors(q, K):
+    K = np.asarray(K)
+    x = np.fmod(np.float32(2) * q, (2 * K).astype(np.float32)).astype(np.float32)
+    c, r, s = _reduce(x)
+    # candidates in original coordinates: k_i = c_i + s_i * p_{r_i}
+    def lift(P):
+        pr = P[:, r]                    # [ncand, n, 8]: p_{r_i}
+        pr = np.transpose(pr, (1, 0, 2))
+        return c[:, None, :] + s[:, None, :] * pr
+    kS = lift(STRICT)
+    dS = _recipe(x, kS)
+    out_slots = np.full((q.shape[0], 32), -1, np.int64)
+    suspects = 0
+    for l in range(q.shape[0]):
+        d, k = dS[l], kS[l]
+        keep = d < np.float32(8)
+        n8 = keep.sum()
+        dd = np.sort(d[keep])
+        suspect = n8 <= 32 or dd[31] >= np.float32(7.999)
+        if suspect:
+            suspects += 1
+            kB = c[l] + s[l] * BOUNDARY[:, r[l]]
+            dB = _recipe(x[l:l + 1], kB[None])[0]
+            d = np.concatenate([d, dB])
+            k = np.concatenate([k, kB])
+            keep = d < np.float32(8)
+        d, k = d[keep], k[keep]
+        slot = oracle.locations(k.astype(np.int32), K).astype(np.int64)
+        bits = d.view(np.uint32).astype(np.int64)
+        order = np.lexsort(tuple(k[:, i] for i in range(7, -1, -1)) + (slot, bits))[:32]
+        out_slots[l, :order.size] = slot[order]
+    return out_slots, suspects
+
+
+def test_candidate_table_shape():
+    """Sec. 2.6: exactly 232 lattice points lie within sqrt 8 of F."""
+    assert STRICT.shape == (232, 8)
+    norms = (STRICT ** 2).sum(1)
+    assert sorted(np.unique(norms)) == [0, 8, 16]
+    assert [(norms == v).sum() for v in (0, 8, 16)] == [1, 149, 82]
+    for P in (STRICT, BOUNDARY):
+        assert np.all(P.sum(1) % 4 == 0)
+        assert np.all((P % 2 == 0).all(1) | (P % 2 == 1).all(1))
+    assert len({tuple(v) for v in np.concatenate([STRICT, BOUNDARY])}) == 232 + BOUNDARY.shape[0]
+
+
+def test_generator_reproduces_committed_table():
+    import importlib.util
+    spec = importlib.util.spec_from_file_location(
+        "gen", os.path.join(ROOT, "paper_2107_03474_amd", "csrc", "gen_e8_candidates.py"))
+    gen = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(gen)
+    info = gen.main(write=False)
+    np.testing.assert_array_equal(info["strict"], STRICT)
+    np.testing.assert_array_equal(info["boundary"], BOUNDARY)
+    assert info["gap"] > 0.5
+
+
+@pytest.mark.parametrize("K", [(4,) * 8, (8,) * 8, (14,) * 8, (2, 4, 6, 8, 2, 4, 6, 8), (2,) * 8])
+def test_model_matches_oracle(K):
+    rng = np.random.default_rng(99)
+    n = 1500
+    q = (rng.random((n, 8)) * np.asarray(K)).astype(np.float32)
+    q[:100] -= np.asarray(K, np.float32) * 3          # far outside: exercises the wrap
+    slots, _ = model_neighbors(q, K)
+    nb = oracle.neighbors(q, K)
+    np.testing.assert_array_equal(slots, nb["slot"])
+
+
+def test_model_special_points():
+    K = (8,) * 8
+    rho = np.array([0, 1, 2, 3, 4, 5, 6, 23], np.float32)
+    pts = [np.zeros(8), np.full(8, 0.5), [1, 0, 0, 0, 0, 0, 0, 0], [0.5] * 7 + [-0.5],
+           2.0 ** -11 * rho, np.full(8, 0.5) + 2.0 ** -11 * rho, [1, 1, 0, 0, 0, 0, 0, 0.0],
+           [0.25, 0.25, 0.25, 0.25, 0, 0, 0, 0], [0.5, 0.5, 0.5, 0.5, 0.5, 0.5, 0.5, 1.0]]
+    q = np.mod(np.array(pts, np.float64), 8).astype(np.float32)
+    slots, suspects = model_neighbors(q, K)
+    nb = oracle.neighbors(q, K)
+    np.testing.assert_array_equal(slots, nb["slot"])
+    assert suspects >= 3
