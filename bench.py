@@ -89,6 +89,23 @@ def cpu_baseline(oracle, W, w, q_np, table, G, target_s, torch):
                       % (n, w.name, t, t_nb, t_alg)}
 
 
+def measured_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter summary
+    (FETCH_SIZE and WRITE_SIZE, copy-calibrated), or None if there is none or the
+    kernel source changed since the counters were taken."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", "counters_%s.json" % workload)
+    src = os.path.join(ROOT, "paper_2107_03474_amd", "csrc", "lram.hip")
+    try:
+        prof = json.load(open(path))
+        if prof.get("source_sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest():
+            return None
+        return prof["kernels"][kernel]["traffic_bytes"]
+    except (OSError, KeyError, ValueError):
+        return None
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -98,6 +115,8 @@ def main():
     ap.add_argument("--mode", default="atomic", choices=["atomic", "sorted"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy 5 times (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path (each GPU would run the "
@@ -111,6 +130,15 @@ def main():
 
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
+    if args.calibrate_copy:
+        a = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(5):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration": "copy", "bytes_read_per_launch": a.numel() * 4,
+                          "bytes_written_per_launch": a.numel() * 4, "launches": 5}), flush=True)
+        return
     lram.load()
     w, fits = pick_workload(W, args.workload, torch)
     if not fits:
@@ -169,6 +197,7 @@ def main():
     else:
         kname, kms, kbytes, kreq = "k_forward", fwd_ms, fwd_bytes, fwd_req
     achieved = kbytes / (kms * 1e-3) / 1e9
+    traffic = measured_traffic(w.name, kname)
     res = {
         "metric": "lookups/sec fwd and fwd+bwd; achieved HBM GB/s vs peak (1 GPU)",
         "value": L / (ms_step * 1e-3),
@@ -189,7 +218,7 @@ def main():
         "bwd_ms": bwd_ms,
         "distinct_rows": U,
         "roofline": {"kernel": kname, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "bytes_per_launch": kbytes, "requested_bytes_per_launch": kreq,
                      "requested_GBps": kreq / (kms * 1e-3) / 1e9},
         "fwd_hbm_GBps": fwd_bytes / (fwd_ms * 1e-3) / 1e9,

@@ -682,6 +682,19 @@ __global__ void __launch_bounds__(THREADS) k_backward_atomic(const float* __rest
         const float4 gv = *reinterpret_cast<const float4*>(gp + e);
         g[e] = gv.x; g[e + 1] = gv.y; g[e + 2] = gv.z; g[e + 3] = gv.w;
       }
+      // value-gradient scatter: M consecutive lanes own one gradient row, so each
+      // atomic instruction covers 64/M whole rows (full-line requests at L2)
+      if (gtab) {
+        constexpr int RA = WAVE / M;
+        const int col = lane % M;
+        const float gc = gout[(size_t)l * M + col];
+#pragma unroll 4
+        for (int k = 0; k < NB / RA; ++k) {
+          const int j = k * RA + lane / M;
+          const int32_t s = W.nbr[j].slot;
+          if (s >= 0) unsafeAtomicAdd(gtab + (size_t)s * M + col, W.wgt[j] * gc);
+        }
+      }
       uint4 v[G::NP];
       int32_t sl[G::NP];
 #pragma unroll
@@ -694,17 +707,11 @@ __global__ void __launch_bounds__(THREADS) k_backward_atomic(const float* __rest
 #pragma unroll
       for (int p = 0; p < G::NP; ++p) {
         const int j = p * G::RPP + rsub;
-        const float wj = W.wgt[j];
         float f[G::EPC];
         unpack16<DT, G::EPC>(v[p], f);
         float pd = 0.0f;
 #pragma unroll
         for (int e = 0; e < G::EPC; ++e) pd = fmaf(g[e], f[e], pd);
-        if (sl[p] >= 0 && gtab) {
-          float* dst = gtab + (size_t)sl[p] * M + ch * G::EPC;
-#pragma unroll
-          for (int e = 0; e < G::EPC; ++e) unsafeAtomicAdd(dst + e, wj * g[e]);
-        }
         // <G, v_j>: sum over the LPR lanes of this row
 #pragma unroll
         for (int mask = 1; mask < G::LPR; mask <<= 1) pd += __shfl_xor(pd, mask);

@@ -182,7 +182,8 @@ def test_backward_accumulates():
     gt2 = gt1.clone()
     lram.backward(q, table, K, G, grad_table=gt2, want_grad_q=False)
     torch.cuda.synchronize()
-    np.testing.assert_allclose(gt2.cpu().numpy(), 2 * gt1.cpu().numpy(), rtol=1e-6, atol=1e-9)
+    # atomic accumulation order varies between calls: compare at the fp32 parity bar
+    np.testing.assert_allclose(gt2.cpu().numpy(), 2 * gt1.cpu().numpy(), rtol=1e-5, atol=1e-7)
 
 
 @pytest.mark.parametrize("name", ["k4-m32-f32-uniform", "k4-m32-f32-gmm64"])
