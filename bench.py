@@ -115,6 +115,7 @@ def main():
     ap.add_argument("--mode", default="atomic", choices=["atomic", "sorted"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-compare", action="store_true", help="skip timing the other scatter mode")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (HBM counter calibration)")
     args = ap.parse_args()
@@ -186,6 +187,25 @@ def main():
     ms_step = wall * 1e3 / args.steps
     log("timed %d steps: %.3f ms/step (forward %.3f ms, backward %.3f ms)" % (args.steps, ms_step, fwd_ms, bwd_ms))
 
+    # the other value-gradient scatter, timed the same way for comparison (not part of `value`)
+    other = "sorted" if args.mode == "atomic" else "atomic"
+    other_ms = None
+    if not args.no_compare:
+        ws = None
+        if other == "sorted":
+            ws = torch.empty(lram.backward_workspace_bytes(w.B, w.H, w.m, "sorted"), dtype=torch.uint8, device=dev)
+        lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, mode=other, workspace=ws)
+        torch.cuda.synchronize()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        e[0].record(stream)
+        for _ in range(5):
+            lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, mode=other, workspace=ws)
+        e[1].record(stream)
+        torch.cuda.synchronize()
+        other_ms = e[0].elapsed_time(e[1]) / 5
+        del ws
+        log("backward with the %s scatter: %.3f ms" % (other, other_ms))
+
     st = 4 if w.dtype == "f32" else 2
     L = w.L
     fwd_bytes = L * (32 + w.m * st) + U * w.m * st
@@ -216,6 +236,7 @@ def main():
         "fwd_lookups_per_s": L / (fwd_ms * 1e-3),
         "fwd_ms": fwd_ms,
         "bwd_ms": bwd_ms,
+        "bwd_ms_by_scatter": {args.mode: bwd_ms, other: other_ms},
         "distinct_rows": U,
         "roofline": {"kernel": kname, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,

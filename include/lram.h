@@ -118,8 +118,9 @@ int lram_backward_workspace_bytes(int64_t B, int64_t H, int32_t m, int mode, siz
  *   grad_q[l][i] = sum_j -2 u_j^3 (x_i - k_{j,i}) <grad_out[l], table[slot_j]>,
  *       u_j = 1 - s_j/8 (overwritten; nullable to skip it)
  * The neighbour search is recomputed from q.  workspace/ws_bytes: device
- * buffer of at least lram_backward_workspace_bytes (may be NULL for the atomic
- * mode).  grad_table may be NULL only if grad_q is not.
+ * buffer, 256-byte aligned, of at least lram_backward_workspace_bytes (may be
+ * NULL for the atomic mode); its contents on entry do not matter.  The sorted
+ * mode needs 32 L < 2^32.  grad_table may be NULL only if grad_q is not.
  */
 int lram_backward(const float* q, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
                   int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_q, int mode,

@@ -23,6 +23,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <utility>
+
 #include "../../include/lram.h"
 #include "e8_candidates.inc"
 
@@ -646,14 +648,17 @@ __global__ void __launch_bounds__(THREADS) k_forward(const float* __restrict__ q
   }
 }
 
-// Backward with the value-gradient scatter done by fp32 atomics, fused with
-// the query gradient: per lookup, read the 32 rows once for <G, v_j>, add
-// w_j G into grad_table[slot_j], and form dq from the coordinate errors.
-template <int DT, int M>
-__global__ void __launch_bounds__(THREADS) k_backward_atomic(const float* __restrict__ q, Params P,
-                                                             const void* __restrict__ table,
-                                                             const float* __restrict__ gout,
-                                                             float* __restrict__ gtab, float* __restrict__ gq) {
+// Backward, fused with the query gradient: per lookup, read the 32 rows once
+// for <G, v_j> and form dq from the coordinate errors.  The value gradient is
+// either added straight into grad_table with fp32 atomics (EMIT = false), or
+// emitted as (location, (lookup, w_j)) pairs for the sorted segmented
+// reduction (EMIT = true; padding gets the key N, which sorts last).
+template <int DT, int M, bool EMIT>
+__global__ void __launch_bounds__(THREADS) k_backward(const float* __restrict__ q, Params P,
+                                                      const void* __restrict__ table,
+                                                      const float* __restrict__ gout, float* __restrict__ gtab,
+                                                      float* __restrict__ gq, uint32_t* __restrict__ pair_key,
+                                                      uint2* __restrict__ pair_val) {
   using G = RowGeom<DT, M>;
   constexpr int ICOORD = G::LPR >= 8 ? 1 : 8 / G::LPR;  // query coordinates per lane
   __shared__ BlockLds S;
@@ -684,7 +689,7 @@ __global__ void __launch_bounds__(THREADS) k_backward_atomic(const float* __rest
       }
       // value-gradient scatter: M consecutive lanes own one gradient row, so each
       // atomic instruction covers 64/M whole rows (full-line requests at L2)
-      if (gtab) {
+      if (!EMIT && gtab) {
         constexpr int RA = WAVE / M;
         const int col = lane % M;
         const float gc = gout[(size_t)l * M + col];
@@ -730,6 +735,11 @@ __global__ void __launch_bounds__(THREADS) k_backward_atomic(const float* __rest
         }
       }
     }
+    if (EMIT && gtab && lane < NB) {
+      const int32_t sl = W.nbr[lane].slot;
+      pair_key[l * NB + lane] = sl >= 0 ? (uint32_t)sl : P.N;
+      pair_val[l * NB + lane] = make_uint2((uint32_t)l, __float_as_uint(W.wgt[lane]));
+    }
     if (gq) {
 #pragma unroll
       for (int mask = G::LPR; mask < WAVE; mask <<= 1)
@@ -744,6 +754,234 @@ __global__ void __launch_bounds__(THREADS) k_backward_atomic(const float* __rest
       }
     }
     wave_lds_sync();
+  }
+}
+
+
+// ---------------------------------------------------------------------------
+// Sorted value-gradient scatter: a stable LSD radix sort of the (location,
+// (lookup, weight)) pairs by location, then a segmented reduction that writes
+// every touched gradient row with one read-modify-write.
+
+constexpr int RADIX_BITS = 8;
+constexpr int RADIX = 1 << RADIX_BITS;
+constexpr int SORT_ROUNDS = 16;                    // elements per thread per tile
+constexpr int SORT_TILE = THREADS * SORT_ROUNDS;   // 4096
+constexpr int SCAN_TILE = THREADS * 16;            // 4096 entries per scan block
+
+// hist[d * nblocks + b] = number of keys in tile b whose digit is d
+__global__ void __launch_bounds__(THREADS) k_radix_hist(const uint32_t* __restrict__ keys, int64_t n, int shift,
+                                                        uint32_t* __restrict__ hist, int nblocks) {
+  __shared__ uint32_t h[RADIX];
+  const int t = threadIdx.x;
+  h[t] = 0;
+  __syncthreads();
+  const int64_t base = (int64_t)blockIdx.x * SORT_TILE;
+#pragma unroll 4
+  for (int r = 0; r < SORT_ROUNDS; ++r) {
+    const int64_t i = base + r * THREADS + t;
+    if (i < n) atomicAdd(&h[(keys[i] >> shift) & (RADIX - 1)], 1u);
+  }
+  __syncthreads();
+  hist[(int64_t)t * nblocks + blockIdx.x] = h[t];
+}
+
+// Exclusive scan, three kernels: per-block scan with block totals, scan of the
+// totals (one block), add the scanned totals back.
+__global__ void __launch_bounds__(THREADS) k_scan_blocks(uint32_t* __restrict__ a, int64_t n,
+                                                         uint32_t* __restrict__ totals) {
+  __shared__ uint32_t part[THREADS];
+  const int t = threadIdx.x;
+  const int64_t base = (int64_t)blockIdx.x * SCAN_TILE + (int64_t)t * 16;
+  uint32_t v[16];
+  uint32_t sum = 0;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    v[k] = base + k < n ? a[base + k] : 0u;
+    sum += v[k];
+  }
+  part[t] = sum;
+  __syncthreads();
+  for (int off = 1; off < THREADS; off <<= 1) {
+    const uint32_t x = t >= off ? part[t - off] : 0u;
+    __syncthreads();
+    part[t] += x;
+    __syncthreads();
+  }
+  uint32_t run = part[t] - sum;  // exclusive prefix of this thread's 16 entries
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    if (base + k < n) a[base + k] = run;
+    run += v[k];
+  }
+  if (t == THREADS - 1) totals[blockIdx.x] = part[t];
+}
+
+__global__ void __launch_bounds__(THREADS) k_scan_totals(uint32_t* __restrict__ totals, int64_t n) {
+  __shared__ uint32_t part[THREADS];
+  __shared__ uint32_t carry;
+  const int t = threadIdx.x;
+  if (t == 0) carry = 0;
+  __syncthreads();
+  for (int64_t base = 0; base < n; base += THREADS) {
+    const uint32_t v = base + t < n ? totals[base + t] : 0u;
+    part[t] = v;
+    __syncthreads();
+    for (int off = 1; off < THREADS; off <<= 1) {
+      const uint32_t x = t >= off ? part[t - off] : 0u;
+      __syncthreads();
+      part[t] += x;
+      __syncthreads();
+    }
+    if (base + t < n) totals[base + t] = carry + part[t] - v;
+    __syncthreads();
+    if (t == THREADS - 1) carry += part[t];
+    __syncthreads();
+  }
+}
+
+__global__ void __launch_bounds__(THREADS) k_scan_add(uint32_t* __restrict__ a, int64_t n,
+                                                      const uint32_t* __restrict__ totals) {
+  const uint32_t add = totals[blockIdx.x];
+  const int64_t base = (int64_t)blockIdx.x * SCAN_TILE;
+#pragma unroll 4
+  for (int k = 0; k < 16; ++k) {
+    const int64_t i = base + k * THREADS + threadIdx.x;
+    if (i < n) a[i] += add;
+  }
+}
+
+// Stable scatter of one radix pass.  Element order inside a tile is (round,
+// wave, lane), i.e. index order; ranks among equal digits come from an 8-ballot
+// match inside the wave plus per-(wave, digit) counts carried across rounds.
+__global__ void __launch_bounds__(THREADS) k_radix_scatter(const uint32_t* __restrict__ kin,
+                                                           const uint2* __restrict__ vin, int64_t n, int shift,
+                                                           const uint32_t* __restrict__ offs, int nblocks,
+                                                           uint32_t* __restrict__ kout, uint2* __restrict__ vout) {
+  __shared__ uint32_t run_cnt[RADIX];
+  __shared__ uint32_t wave_cnt[WAVES][RADIX];
+  __shared__ uint32_t base_off[RADIX];
+  const int t = threadIdx.x, w = t / WAVE, lane = t % WAVE;
+  run_cnt[t] = 0;
+  base_off[t] = offs[(int64_t)t * nblocks + blockIdx.x];
+#pragma unroll
+  for (int k = 0; k < WAVES; ++k) wave_cnt[k][t] = 0;
+  __syncthreads();
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (WAVE - lane));
+  const int64_t base = (int64_t)blockIdx.x * SORT_TILE;
+  for (int r = 0; r < SORT_ROUNDS; ++r) {
+    const int64_t i = base + r * THREADS + t;
+    const bool valid = i < n;
+    const uint32_t key = valid ? kin[i] : 0u;
+    const uint2 val = valid ? vin[i] : make_uint2(0, 0);
+    const uint32_t d = (key >> shift) & (RADIX - 1);
+    uint64_t match = __ballot(valid);
+#pragma unroll
+    for (int b = 0; b < RADIX_BITS; ++b) {
+      const bool bit = (d >> b) & 1u;
+      const uint64_t bb = __ballot(bit);
+      match &= bit ? bb : ~bb;
+    }
+    const int rank = __popcll(match & lt);
+    if (valid && rank == 0) wave_cnt[w][d] = (uint32_t)__popcll(match);
+    __syncthreads();
+    {
+      uint32_t run = run_cnt[t];
+#pragma unroll
+      for (int k = 0; k < WAVES; ++k) {
+        const uint32_t c = wave_cnt[k][t];
+        wave_cnt[k][t] = run;
+        run += c;
+      }
+      run_cnt[t] = run;
+    }
+    __syncthreads();
+    if (valid) {
+      const uint32_t pos = base_off[d] + wave_cnt[w][d] + (uint32_t)rank;
+      kout[pos] = key;
+      vout[pos] = val;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < WAVES; ++k) wave_cnt[k][t] = 0;
+    __syncthreads();
+  }
+}
+
+// Segmented reduction of the sorted pairs: one wave per 64 consecutive pairs
+// (lane = pair).  Each lane forms w * G[lookup] in column groups of 16, a
+// segmented inclusive scan over the lanes sums every run of equal locations,
+// and the last lane of each run writes the row: a plain read-modify-write when
+// the whole run lies inside these 64 pairs (no other wave touches that row),
+// fp32 atomics for the runs cut by the chunk edges.
+template <int M>
+__global__ void __launch_bounds__(THREADS) k_segreduce(const uint32_t* __restrict__ keys,
+                                                       const uint2* __restrict__ vals, int64_t n, uint32_t N,
+                                                       const float* __restrict__ gout, float* __restrict__ gtab) {
+  const int lane = threadIdx.x % WAVE;
+  const int64_t chunk = (int64_t)blockIdx.x * WAVES + threadIdx.x / WAVE;
+  const int64_t p = chunk * WAVE + lane;
+  if (chunk * WAVE >= n) return;
+  const bool valid = p < n;
+  const uint32_t key = valid ? keys[p] : N;
+  const uint2 val = valid ? vals[p] : make_uint2(0, 0);
+  const uint32_t prev_edge = (lane == 0 && p > 0 && valid) ? keys[p - 1] : 0xFFFFFFFFu;
+  const int64_t pl = chunk * WAVE + WAVE;  // first pair of the next chunk
+  const uint32_t next_edge = (lane == WAVE - 1 && pl < n) ? keys[pl] : 0xFFFFFFFFu;
+  const uint32_t up = __shfl_up(key, 1);
+  const uint32_t down = __shfl_down(key, 1);
+  const bool head = (lane == 0) ? (p == 0 || prev_edge != key) : (up != key);
+  const bool tail = (lane == WAVE - 1) ? (next_edge != key) : (down != key);
+  const bool live = valid && key < N;
+  // head flags of the segmented scan (shared by every column group)
+  bool seen = head;
+  {
+    bool f = head;
+#pragma unroll
+    for (int off = 1; off < WAVE; off <<= 1) {
+      const bool fo = __shfl_up((int)f, off) != 0;
+      if (lane >= off) f = f || fo;
+    }
+    seen = f;  // a head of this lane's run lies inside the chunk at or before this lane
+  }
+  const bool writer = live && (tail || lane == WAVE - 1);
+  const bool partial = !seen || (lane == WAVE - 1 && !tail);
+  const float wgt = __uint_as_float(val.y);
+  const float* gp = gout + (size_t)val.x * M;
+  float* dst = gtab + (size_t)key * M;
+#pragma unroll 1
+  for (int c0 = 0; c0 < M; c0 += 16) {
+    float v[16];
+#pragma unroll
+    for (int e = 0; e < 16; e += 4) {
+      const float4 g = live ? *reinterpret_cast<const float4*>(gp + c0 + e) : make_float4(0, 0, 0, 0);
+      v[e] = wgt * g.x; v[e + 1] = wgt * g.y; v[e + 2] = wgt * g.z; v[e + 3] = wgt * g.w;
+    }
+    bool f = head;
+#pragma unroll
+    for (int off = 1; off < WAVE; off <<= 1) {
+      const bool fo = __shfl_up((int)f, off) != 0;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const float o = __shfl_up(v[e], off);
+        if (lane >= off && !f) v[e] += o;
+      }
+      if (lane >= off) f = f || fo;
+    }
+    if (writer) {
+      if (partial) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) unsafeAtomicAdd(dst + c0 + e, v[e]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 16; e += 4) {
+          float4* d4 = reinterpret_cast<float4*>(dst + c0 + e);
+          float4 o = *d4;
+          o.x += v[e]; o.y += v[e + 1]; o.z += v[e + 2]; o.w += v[e + 3];
+          *d4 = o;
+        }
+      }
+    }
   }
 }
 
@@ -813,12 +1051,81 @@ struct FwdLaunch {
   }
 };
 
+// Workspace of the sorted scatter for n = 32 L pairs (each piece 256-byte aligned).
+struct SortWs {
+  uint32_t *k0, *k1, *hist, *totals;
+  uint2 *v0, *v1;
+  int64_t n;
+  int nblocks;
+  int64_t nh, nbt;
+};
+
+size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
+
+size_t sort_ws_layout(int64_t L, SortWs* ws, char* base) {
+  const int64_t n = L * NB;
+  const int nblocks = (int)((n + SORT_TILE - 1) / SORT_TILE);
+  const int64_t nh = (int64_t)RADIX * nblocks;
+  const int64_t nbt = (nh + SCAN_TILE - 1) / SCAN_TILE;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    char* ptr = base ? base + off : nullptr;
+    off += align256(bytes);
+    return ptr;
+  };
+  char* k0 = take(n * 4);
+  char* k1 = take(n * 4);
+  char* v0 = take(n * 8);
+  char* v1 = take(n * 8);
+  char* h = take(nh * 4);
+  char* tt = take(nbt * 4);
+  if (ws) {
+    ws->k0 = (uint32_t*)k0; ws->k1 = (uint32_t*)k1; ws->v0 = (uint2*)v0; ws->v1 = (uint2*)v1;
+    ws->hist = (uint32_t*)h; ws->totals = (uint32_t*)tt;
+    ws->n = n; ws->nblocks = nblocks; ws->nh = nh; ws->nbt = nbt;
+  }
+  return off;
+}
+
 template <int DT, int M>
 struct BwdAtomicLaunch {
   static int go(const float* q, const Params& P, const void* table, const float* g, float* gt, float* gq,
                 hipStream_t s) {
-    hipLaunchKernelGGL((k_backward_atomic<DT, M>), dim3(grid_for(P.L)), dim3(THREADS), 0, s, q, P, table, g,
-                       gt, gq);
+    hipLaunchKernelGGL((k_backward<DT, M, false>), dim3(grid_for(P.L)), dim3(THREADS), 0, s, q, P, table, g,
+                       gt, gq, (uint32_t*)nullptr, (uint2*)nullptr);
+    return launched();
+  }
+};
+
+template <int DT, int M>
+struct BwdSortedLaunch {
+  static int go(const float* q, const Params& P, const void* table, const float* g, float* gt, float* gq,
+                const SortWs& ws, hipStream_t s) {
+    hipLaunchKernelGGL((k_backward<DT, M, true>), dim3(grid_for(P.L)), dim3(THREADS), 0, s, q, P, table, g, gt,
+                       gq, ws.k0, ws.v0);
+    int rc = launched();
+    if (rc || !gt) return rc;
+    int bits = 0;
+    while (bits < 32 && (P.N >> bits) != 0) ++bits;  // keys lie in [0, N]
+    uint32_t* kin = ws.k0;
+    uint32_t* kout = ws.k1;
+    uint2* vin = ws.v0;
+    uint2* vout = ws.v1;
+    for (int shift = 0; shift < bits; shift += RADIX_BITS) {
+      hipLaunchKernelGGL(k_radix_hist, dim3(ws.nblocks), dim3(THREADS), 0, s, kin, ws.n, shift, ws.hist,
+                         ws.nblocks);
+      hipLaunchKernelGGL(k_scan_blocks, dim3((unsigned)ws.nbt), dim3(THREADS), 0, s, ws.hist, ws.nh, ws.totals);
+      hipLaunchKernelGGL(k_scan_totals, dim3(1), dim3(THREADS), 0, s, ws.totals, ws.nbt);
+      hipLaunchKernelGGL(k_scan_add, dim3((unsigned)ws.nbt), dim3(THREADS), 0, s, ws.hist, ws.nh, ws.totals);
+      hipLaunchKernelGGL(k_radix_scatter, dim3(ws.nblocks), dim3(THREADS), 0, s, kin, vin, ws.n, shift, ws.hist,
+                         ws.nblocks, kout, vout);
+      if ((rc = launched())) return rc;
+      std::swap(kin, kout);
+      std::swap(vin, vout);
+    }
+    const unsigned chunks = (unsigned)((ws.n + WAVE - 1) / WAVE);
+    hipLaunchKernelGGL((k_segreduce<M>), dim3((chunks + WAVES - 1) / WAVES), dim3(THREADS), 0, s, kin, vin, ws.n,
+                       P.N, g, gt);
     return launched();
   }
 };
@@ -876,6 +1183,11 @@ int lram_backward_workspace_bytes(int64_t B, int64_t H, int32_t m, int mode, siz
     *bytes = 0;
     return LRAM_OK;
   }
+  if (mode == LRAM_SCATTER_SORTED) {
+    if (H != 0 && B > INT64_MAX / H / NB) return LRAM_EINVAL;
+    *bytes = sort_ws_layout(B * H, nullptr, nullptr);
+    return LRAM_OK;
+  }
   return LRAM_EMODE;
 }
 
@@ -890,12 +1202,19 @@ int lram_backward(const float* q, int64_t B, int64_t H, const int32_t K[8], cons
   if (rc) return rc;
   rc = check_table(table, dtype, N, m, P, L);
   if (rc) return rc;
-  if (mode != LRAM_SCATTER_ATOMIC) return LRAM_EMODE;
+  if (mode != LRAM_SCATTER_ATOMIC && mode != LRAM_SCATTER_SORTED) return LRAM_EMODE;
   if (L == 0) return LRAM_OK;
   if (!grad_out || (reinterpret_cast<uintptr_t>(grad_out) & 15)) return LRAM_EINVAL;
   if (!grad_table && !grad_q) return LRAM_EINVAL;
   if (grad_table && (reinterpret_cast<uintptr_t>(grad_table) & 15)) return LRAM_EINVAL;
-  return dispatch<BwdAtomicLaunch>(dtype, m, q, P, table, grad_out, grad_table, grad_q, (hipStream_t)stream);
+  if (mode == LRAM_SCATTER_ATOMIC)
+    return dispatch<BwdAtomicLaunch>(dtype, m, q, P, table, grad_out, grad_table, grad_q, (hipStream_t)stream);
+  if (L > INT64_MAX / NB || L * NB >= (int64_t(1) << 32)) return LRAM_EINVAL;  // positions are 32-bit
+  const size_t need = sort_ws_layout(L, nullptr, nullptr);
+  if (!workspace || ws_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LRAM_EWORKSPACE;
+  SortWs ws;
+  sort_ws_layout(L, &ws, reinterpret_cast<char*>(workspace));
+  return dispatch<BwdSortedLaunch>(dtype, m, q, P, table, grad_out, grad_table, grad_q, ws, (hipStream_t)stream);
 }
 
 }  // extern "C"

@@ -87,6 +87,8 @@ def test_backward_validation(lib):
     n = ctypes.c_size_t(123)
     assert lib.lram_backward_workspace_bytes(4, 1, 32, 0, ctypes.byref(n)) == 0 and n.value == 0
     assert lib.lram_backward_workspace_bytes(4, 1, 32, 9, ctypes.byref(n)) == 5
+    assert lib.lram_backward_workspace_bytes(4, 1, 32, 1, ctypes.byref(n)) == 0 and n.value >= 4 * 32 * 24
+    assert bwd(mode=1, ws=None) == 4  # sorted mode without a workspace
     assert lib.lram_backward_workspace_bytes(4, 1, 48, 0, ctypes.byref(n)) == 3
 
 

@@ -135,11 +135,12 @@ def _tol(dtype):
     return 1e-5 if dtype == torch.float32 else 2e-2
 
 
+@pytest.mark.parametrize("mode", ["atomic", "sorted"])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("m", [32, 64])
 @pytest.mark.parametrize("K", [(4,) * 8, (2, 4, 6, 8, 2, 4, 6, 8)])
-def test_forward_backward_small(K, m, dtype):
-    _say("fwd/bwd K=%s m=%d %s" % (K, m, dtype))
+def test_forward_backward_small(K, m, dtype, mode):
+    _say("fwd/bwd K=%s m=%d %s %s" % (K, m, dtype, mode))
     rng = np.random.default_rng(11)
     L = 3000
     q_np = (rng.random((L, 8)) * np.asarray(K)).astype(np.float32)
@@ -149,7 +150,7 @@ def test_forward_backward_small(K, m, dtype):
     table = _small_table(K, m, dtype)
     G = torch.randn((L, m), device=DEV, dtype=torch.float32)
     out = lram.forward(q, table, K)
-    gt, gq = lram.backward(q, table, K, G)
+    gt, gq = lram.backward(q, table, K, G, mode=mode)
     torch.cuda.synchronize()
     nb = oracle.neighbors(q_np, K)
     tab = table.float().cpu().numpy()
@@ -186,17 +187,18 @@ def test_backward_accumulates():
     np.testing.assert_allclose(gt2.cpu().numpy(), 2 * gt1.cpu().numpy(), rtol=1e-5, atol=1e-7)
 
 
+@pytest.mark.parametrize("mode", ["atomic", "sorted"])
 @pytest.mark.parametrize("name", ["k4-m32-f32-uniform", "k4-m32-f32-gmm64"])
-def test_workload_full_parity(name):
+def test_workload_full_parity(name, mode):
     """Small workloads in full: every lookup, every output."""
     w = W.WORKLOADS[name]
-    _say("full parity", name)
+    _say("full parity", name, mode)
     q_np = W.queries(w)
     q = torch.from_numpy(q_np).to(DEV)
     table = W.make_table(w, DEV)
     G = W.grad_out(w, DEV)
     out = lram.forward(q, table, w.K)
-    gt, gq = lram.backward(q, table, w.K, G)
+    gt, gq = lram.backward(q, table, w.K, G, mode=mode)
     torch.cuda.synchronize()
     nb = oracle.neighbors(q_np, w.K)
     rows = oracle.gather_rows(table.float().cpu().numpy(), nb["slot"])
@@ -210,3 +212,42 @@ def test_workload_full_parity(name):
     mask = np.ones(w.N, bool)
     mask[uniq] = False
     assert np.all(dV[mask] == 0)
+
+
+@pytest.mark.parametrize("mode", ["atomic", "sorted"])
+def test_hot_rows(mode):
+    """Many lookups on a few lattice cells: runs of one location span many
+    64-pair chunks of the sorted reduction (and contend in the atomic one)."""
+    _say("hot rows", mode)
+    K = (8,) * 8
+    rng = np.random.default_rng(13)
+    centres = (rng.random((3, 8)) * 8)
+    L = 20000
+    q_np = (centres[rng.integers(0, 3, L)] + 0.05 * rng.standard_normal((L, 8))).astype(np.float32)
+    q = torch.from_numpy(q_np).to(DEV)
+    table = _small_table(K, 32, torch.float32)
+    G = torch.randn((L, 32), device=DEV)
+    gt, gq = lram.backward(q, table, K, G, mode=mode)
+    torch.cuda.synchronize()
+    nb = oracle.neighbors(q_np, K)
+    uniq, acc = oracle.grad_table_rows(nb, G.cpu().numpy())
+    dV = gt.cpu().numpy()
+    assert uniq.size < 600
+    assert _rel_rows(dV[uniq], acc).max() <= 1e-5
+    mask = np.ones(dV.shape[0], bool)
+    mask[uniq] = False
+    assert np.all(dV[mask] == 0)
+    rows = oracle.gather_rows(table.cpu().numpy(), nb["slot"])
+    assert _rel_rows(gq.cpu().numpy(), oracle.grad_query(nb, rows, G.cpu().numpy())).max() <= 1e-4
+
+
+def test_sorted_workspace_errors():
+    K = (4,) * 8
+    q = torch.rand((100, 8), device=DEV) * 4
+    table = _small_table(K, 32, torch.float32)
+    G = torch.randn((100, 32), device=DEV)
+    need = lram.backward_workspace_bytes(100, 1, 32, "sorted")
+    assert need > 100 * 32 * 24
+    small = torch.empty(need - 256, dtype=torch.uint8, device=DEV)
+    with pytest.raises(lram.LramError):
+        lram.backward(q, table, K, G, mode="sorted", workspace=small)
