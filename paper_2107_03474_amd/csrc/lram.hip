@@ -5,19 +5,20 @@
 // kernel f(r) = (1 - r^2/8)^4 (Sec. 2.5), truncated to the 32 closest points
 // and found through the symmetry reduction of Sec. 2.6, plus its backward.
 //
-// Work decomposition (one wave = 64 lanes):
+// Work decomposition (one wave = 64 lanes, up to 64 lookups per wave):
 //   phase A  lane-per-lookup: wrap, E8 closest point (D8 and D8+1/2 decoders
 //            with a parity fix), and the signed permutation that carries the
-//            offset into the fundamental region F; the result (a "frame") goes
-//            to LDS, 64 lookups per wave.
+//            offset into the fundamental region F; the result (a 64-byte
+//            "frame") goes to LDS.
 //   phase B  wave-per-lookup: the wave builds three 8x8 per-query tables in LDS
 //            (squared coordinate error, location contribution, coordinate
 //            error) indexed by (original coordinate, candidate coordinate
 //            value), scans the 232 candidate points of F (4 per lane) with one
 //            v_perm + one LDS read per coordinate, selects the closest 32 with
 //            ballot/popcount bisection on the fp32 distance bits, and then
-//            gather-reduces (forward) or scatters and forms dq (backward) with
-//            coalesced 16-byte row reads.
+//            gather-reduces (forward) or scatters and forms dq (backward).
+//            The row loads of lookup t are in flight while the wave searches
+//            lookup t+1 (neighbour lists are double-buffered).
 // No MFMA: the path is a gather / scatter bound by HBM, not a contraction.
 
 #include <hip/hip_runtime.h>
@@ -41,12 +42,13 @@ constexpr int CMIN = E8_CAND_MIN;
 constexpr int NV = E8_CAND_MAX - E8_CAND_MIN + 1;
 static_assert(NV == 8, "each per-query table row holds the 8 possible candidate coordinate values");
 static_assert(WAVES <= 4, "the wave index is folded into byte-sized LDS offsets");
+constexpr int KMAX = 8192;  // per-coordinate torus side bound: lattice coordinates fit in int16
 
 // ties at the 32nd distance involve points of the support (at most 121 of them)
 constexpr int TIE_MAX = 128;
-constexpr uint32_t KEY_INF = 0x7F800000u;   // +inf: never selected
-constexpr uint32_t KEY_8 = 0x41000000u;     // 8.0f: support boundary (open ball)
-constexpr uint32_t KEY_4 = 0x40800000u;     // 4.0f: fewer than 32 points are ever closer
+constexpr uint32_t KEY_INF = 0x7F800000u;      // +inf: never selected
+constexpr uint32_t KEY_8 = 0x41000000u;        // 8.0f: support boundary (open ball)
+constexpr uint32_t KEY_4 = 0x40800000u;        // 4.0f: fewer than 32 points are ever closer
 constexpr uint32_t KEY_SUSPECT = 0x40FFF7CFu;  // 7.999f
 
 __constant__ signed char c_strict[E8_NSTRICT][8] = E8_STRICT_INIT;
@@ -57,14 +59,15 @@ struct Params {
   uint32_t S[8];     // mixed-radix strides of the location map, S_7 = 1
   float twoK[8];     // torus side at the Lambda scale
   uint32_t N;
+  int32_t lpw;       // lookups per wave (1..64)
   int64_t L;
 };
 
-// Per-lookup frame written by phase A (112 bytes, 16-byte aligned fields).
+// Per-lookup frame written by phase A (96 bytes).
 struct alignas(16) Frame {
   float x[8];         // Lambda-scale query, wrapped
-  int32_t c[8];       // closest lattice point
-  uint32_t sel[8];    // v_perm selector for original coordinate i: byte r_i of the candidate
+  uint32_t sel[8];    // v_perm selector of original coordinate i: byte r_i (its F position) into byte 0
+  int16_t c[8];       // closest lattice point
   uint32_t misc;      // bits 0-7: sign flips s'_i = -1; bit 8: query finite
   uint32_t pad[3];
 };
@@ -78,9 +81,10 @@ struct alignas(16) Nbr {
 
 struct alignas(16) WaveLds {
   Frame frames[WAVE];
-  Nbr nbr[NB];
-  float wgt[NB];
+  Nbr nbr[2][NB];     // double-buffered: lookup t+1 is searched while t is consumed
+  float wgt[2][NB];
   uint32_t tie[TIE_MAX][2];
+  uint32_t hist[64];  // distance histogram of the selection, 64 buckets on [4, 8)
 };
 
 struct alignas(16) BlockLds {
@@ -98,15 +102,14 @@ __device__ __forceinline__ uint32_t lds_u32(const uint32_t* base, uint32_t byte_
   return *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(base) + byte_off);
 }
 
-__device__ __forceinline__ int lane_id() { return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0)); }
-
 __device__ __forceinline__ int prefix_count(uint64_t mask) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
 }
 
+__device__ __forceinline__ uint32_t uniform(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+
 // Orders LDS traffic between lanes of one wave: the wave's LDS operations
-// execute in issue order, so a compiler barrier plus waiting for the
-// outstanding LDS operations is enough.
+// execute in issue order, so a compiler barrier is enough.
 __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
@@ -116,10 +119,13 @@ __device__ __forceinline__ void wave_lds_sync() {
 __device__ __forceinline__ float bf16_lo(uint32_t v) { return __uint_as_float(v << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t v) { return __uint_as_float(v & 0xFFFF0000u); }
 
-__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (u >> 16) | 0x40u;  // quiet NaN
-  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// two fp32 -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32)
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  f32x2_t v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
 
 // ---------------------------------------------------------------------------
@@ -148,7 +154,7 @@ __device__ __forceinline__ void d8_round(const float (&y)[8], int (&r)[8]) {
   }
 }
 
-__device__ void make_frame(const float* __restrict__ q, bool have, const Params& P, Frame& F) {
+__device__ __forceinline__ void make_frame(const float* __restrict__ q, bool have, const Params P, Frame& F) {
   float x[8];
   bool valid = have;
   if (have) {
@@ -197,93 +203,99 @@ __device__ void make_frame(const float* __restrict__ q, bool have, const Params&
     neg |= (y < 0.0f ? 1u : 0u) << i;
   }
   // rank of |y_i| in descending order (ties by index): F position of coordinate i
-  int r[8];
+  uint32_t sel[8];
+  int last = 0;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     int ri = 0;
 #pragma unroll
     for (int j = 0; j < 8; ++j)
       if (j != i) ri += (a[j] > a[i] || (a[j] == a[i] && j < i)) ? 1 : 0;
-    r[i] = ri;
+    sel[i] = 0x0C0C0C00u | (uint32_t)ri;
+    if (ri == 7) last = i;
   }
   // only even numbers of sign changes are isometries of Lambda: fix the parity
   // on the coordinate that lands last (smallest |y|)
-  if (__popc(neg) & 1) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-      if (r[i] == 7) neg ^= 1u << i;
-  }
+  if (__popc(neg) & 1) neg ^= 1u << last;
   float4* fx = reinterpret_cast<float4*>(F.x);
   fx[0] = make_float4(x[0], x[1], x[2], x[3]);
   fx[1] = make_float4(x[4], x[5], x[6], x[7]);
-  int4* fc = reinterpret_cast<int4*>(F.c);
-  fc[0] = make_int4(c[0], c[1], c[2], c[3]);
-  fc[1] = make_int4(c[4], c[5], c[6], c[7]);
   uint4* fs = reinterpret_cast<uint4*>(F.sel);
-  fs[0] = make_uint4(0x0C0C0C00u | r[0], 0x0C0C0C00u | r[1], 0x0C0C0C00u | r[2], 0x0C0C0C00u | r[3]);
-  fs[1] = make_uint4(0x0C0C0C00u | r[4], 0x0C0C0C00u | r[5], 0x0C0C0C00u | r[6], 0x0C0C0C00u | r[7]);
-  F.misc = neg | (valid ? 0x100u : 0u);
+  fs[0] = make_uint4(sel[0], sel[1], sel[2], sel[3]);
+  fs[1] = make_uint4(sel[4], sel[5], sel[6], sel[7]);
+  uint4 w;
+  w.x = (uint32_t)(uint16_t)c[0] | ((uint32_t)(uint16_t)c[1] << 16);
+  w.y = (uint32_t)(uint16_t)c[2] | ((uint32_t)(uint16_t)c[3] << 16);
+  w.z = (uint32_t)(uint16_t)c[4] | ((uint32_t)(uint16_t)c[5] << 16);
+  w.w = (uint32_t)(uint16_t)c[6] | ((uint32_t)(uint16_t)c[7] << 16);
+  reinterpret_cast<uint4*>(F.c)[0] = w;
+  reinterpret_cast<uint4*>(&F.misc)[0] = make_uint4(neg | (valid ? 0x100u : 0u), 0u, 0u, 0u);
 }
 
 // ---------------------------------------------------------------------------
-// Phase B helpers.
+// Phase B: the neighbour search of one lookup.
 
-// Packed candidate bytes for lane-slot idx of a list: byte j = 4*(p_j - CMIN) + 64*w.
-__device__ __forceinline__ void pack_candidate(const signed char (&p)[8], uint32_t wbyte, uint32_t& lo,
-                                               uint32_t& hi) {
-  lo = hi = 0;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    lo |= ((uint32_t)(4 * (p[j] - CMIN)) + wbyte) << (8 * j);
-    hi |= ((uint32_t)(4 * (p[j + 4] - CMIN)) + wbyte) << (8 * j);
-  }
-}
-
+// Packed candidate bytes: byte j = 4*(p_j - CMIN) + 64*w (the LDS byte offset of
+// table entry (., w, p_j) within a coordinate's 256-byte block).
 template <int LIST>
 __device__ __forceinline__ bool load_candidate(int idx, uint32_t wbyte, uint32_t& lo, uint32_t& hi) {
   constexpr int n = LIST == 0 ? E8_NSTRICT : E8_NBOUNDARY;
-  if (idx >= n) {
-    lo = hi = 0;
-    return false;
-  }
-  signed char p[8];
+  lo = hi = 0;
+  if (idx >= n) return false;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) p[j] = LIST == 0 ? c_strict[idx][j] : c_boundary[idx][j];
-  pack_candidate(p, wbyte, lo, hi);
+  for (int j = 0; j < 4; ++j) {
+    const int pl = LIST == 0 ? c_strict[idx][j] : c_boundary[idx][j];
+    const int ph = LIST == 0 ? c_strict[idx][j + 4] : c_boundary[idx][j + 4];
+    lo |= ((uint32_t)(4 * (pl - CMIN)) + wbyte) << (8 * j);
+    hi |= ((uint32_t)(4 * (ph - CMIN)) + wbyte) << (8 * j);
+  }
   return true;
+}
+
+struct Sel {
+  uint32_t s[8];  // v_perm selectors (uniform): byte r_i of the candidate into byte 0
+  uint32_t misc;  // sign bits, validity
+};
+
+__device__ __forceinline__ Sel read_sel(const Frame& F) {
+  Sel o;
+  const uint4 a = reinterpret_cast<const uint4*>(F.sel)[0];
+  const uint4 b = reinterpret_cast<const uint4*>(F.sel)[1];
+  o.s[0] = uniform(a.x); o.s[1] = uniform(a.y); o.s[2] = uniform(a.z); o.s[3] = uniform(a.w);
+  o.s[4] = uniform(b.x); o.s[5] = uniform(b.y); o.s[6] = uniform(b.z); o.s[7] = uniform(b.w);
+  o.misc = uniform(F.misc);
+  return o;
 }
 
 // Recipe distance^2 of candidate (lo,hi): sum over original coordinates i, in
 // order, of the per-query table entry (x_i - k_i)^2 (already fp32-rounded).
-__device__ __forceinline__ float cand_d2(const float* qt, uint32_t lo, uint32_t hi, const uint32_t (&sel)[8]) {
+__device__ __forceinline__ float cand_d2(const float* qt, uint32_t lo, uint32_t hi, const Sel& sel) {
   float d = 0.0f;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    uint32_t a = __builtin_amdgcn_perm(hi, lo, sel[i]);
-    float v = lds_f32(qt, a + 256u * i);
+    const float v = lds_f32(qt, __builtin_amdgcn_perm(hi, lo, sel.s[i]) + 256u * i);
     d = (i == 0) ? v : d + v;
   }
   return d;
 }
 
-__device__ __forceinline__ int32_t cand_slot(const uint32_t* st, uint32_t lo, uint32_t hi,
-                                             const uint32_t (&sel)[8]) {
+__device__ __forceinline__ int32_t cand_slot(const uint32_t* st, uint32_t lo, uint32_t hi, const Sel& sel) {
   uint32_t m = 0;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) m += lds_u32(st, __builtin_amdgcn_perm(hi, lo, sel[i]) + 256u * i);
+  for (int i = 0; i < 8; ++i) m += lds_u32(st, __builtin_amdgcn_perm(hi, lo, sel.s[i]) + 256u * i);
   return (int32_t)(m >> 1);
 }
 
 // Lexicographic key of the lattice point itself (only consulted between equal
 // (distance, location) pairs, which requires a torus side of 2).
-__device__ __forceinline__ uint32_t cand_liftkey(uint32_t lo, uint32_t hi, const uint32_t (&sel)[8],
-                                                 const Frame& F) {
+__device__ __forceinline__ uint32_t cand_liftkey(uint32_t lo, uint32_t hi, const Sel& sel, const Frame& F) {
   uint32_t key = 0;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    uint32_t a = __builtin_amdgcn_perm(hi, lo, sel[i]);
-    int p = (int)((a & 63u) >> 2) + CMIN;
-    int k = ((F.misc >> i) & 1u) ? F.c[i] - p : F.c[i] + p;
+    const uint32_t a = __builtin_amdgcn_perm(hi, lo, sel.s[i]);
+    const int p = (int)((a & 63u) >> 2) + CMIN;
+    const int c = F.c[i];
+    const int k = ((sel.misc >> i) & 1u) ? c - p : c + p;
     key |= ((uint32_t)(k + 8) & 15u) << (4 * (7 - i));
   }
   return key;
@@ -297,21 +309,21 @@ __device__ __forceinline__ int count_below(const uint32_t (&key)[NS], uint32_t t
   return c;
 }
 
-// Selection of the closest 32 (Sec. 2.6) over NS candidate slots per lane.
-// Result: pick bit s set for each selected slot of this lane; returns the
-// number selected; *suspect is set when a point of the boundary list could
-// enter the selection (the 32nd distance is within 1e-3 of the support edge,
-// or fewer than 32 points are in the support).
+// Threshold selection of the closest 32 (Sec. 2.6) over NS candidate slots per
+// lane.  Returns the number selected; a slot is selected iff key < thr, or
+// key == tie_key and it is among the `need` first of those in (location,
+// lattice point) order (tie_key = KEY_INF when there is no tie).  *suspect is
+// set when a point of the boundary list could enter the selection (the 32nd
+// distance is within 1e-3 of the support edge, or fewer than 32 points are in
+// the support).
 template <int NS>
-__device__ int select32(const uint32_t (&key)[NS], const uint32_t (&lo)[NS], const uint32_t (&hi)[NS],
-                        const uint32_t (&sel)[8], const Frame& F, const uint32_t* st, WaveLds& W,
-                        uint32_t& pick, bool& suspect) {
-  const int lane = lane_id();
-  pick = 0;
+__device__ __forceinline__ int threshold32(const uint32_t (&key)[NS], uint32_t& thr, uint32_t& tie_key, int& need,
+                                           bool& suspect) {
+  tie_key = KEY_INF;
+  need = 0;
   const int n8 = count_below(key, KEY_8);
   if (n8 <= NB) {
-#pragma unroll
-    for (int s = 0; s < NS; ++s) pick |= (key[s] < KEY_8 ? 1u : 0u) << s;
+    thr = KEY_8;
     suspect = true;
     return n8;
   }
@@ -320,8 +332,7 @@ __device__ int select32(const uint32_t (&key)[NS], const uint32_t (&lo)[NS], con
   uint32_t lo_k = KEY_4, hi_k = KEY_8;
   int c = count_below(key, lo_k);
   if (c == NB) {
-#pragma unroll
-    for (int s = 0; s < NS; ++s) pick |= (key[s] < lo_k ? 1u : 0u) << s;
+    thr = lo_k;
     suspect = false;
     return NB;
   }
@@ -330,11 +341,10 @@ __device__ int select32(const uint32_t (&key)[NS], const uint32_t (&lo)[NS], con
     lo_k = 0;
   }
   while (hi_k - lo_k > 1) {
-    uint32_t mid = lo_k + ((hi_k - lo_k) >> 1);
+    const uint32_t mid = lo_k + ((hi_k - lo_k) >> 1);
     c = count_below(key, mid);
     if (c == NB) {
-#pragma unroll
-      for (int s = 0; s < NS; ++s) pick |= (key[s] < mid ? 1u : 0u) << s;
+      thr = mid;
       suspect = mid > KEY_SUSPECT;
       return NB;
     }
@@ -343,170 +353,252 @@ __device__ int select32(const uint32_t (&key)[NS], const uint32_t (&lo)[NS], con
     else
       hi_k = mid;
   }
-  // Several candidates share the distance bits lo_k at the 32nd place: take
-  // the ones below, then the tied ones in (location, lattice point) order.
-  const int below = count_below(key, lo_k);
-  const int need = NB - below;
+  // several candidates share the distance bits lo_k at the 32nd place
+  thr = lo_k;
+  tie_key = lo_k;
+  need = NB - count_below(key, lo_k);
   suspect = lo_k > KEY_SUSPECT;
-  int nt = 0;
-#pragma unroll
-  for (int s = 0; s < NS; ++s) {
-    const bool tied = key[s] == lo_k;
-    const uint64_t m = __ballot(tied);
-    const int pos = nt + prefix_count(m);
-    if (tied && pos < TIE_MAX) {
-      W.tie[pos][0] = (uint32_t)cand_slot(st, lo[s], hi[s], sel);
-      W.tie[pos][1] = cand_liftkey(lo[s], hi[s], sel, F);
-    }
-    nt += __popcll(m);
-  }
-  wave_lds_sync();
-#pragma unroll
-  for (int s = 0; s < NS; ++s) {
-    pick |= (key[s] < lo_k ? 1u : 0u) << s;
-    if (key[s] == lo_k) {
-      const uint32_t ms = (uint32_t)cand_slot(st, lo[s], hi[s], sel);
-      const uint32_t mk = cand_liftkey(lo[s], hi[s], sel, F);
-      int rank = 0;
-      const int ntc = nt < TIE_MAX ? nt : TIE_MAX;
-      for (int e = 0; e < ntc; ++e) {
-        const uint32_t es = W.tie[e][0], ek = W.tie[e][1];
-        rank += (es < ms || (es == ms && ek < mk)) ? 1 : 0;
-      }
-      if (rank < need) pick |= 1u << s;
-    }
-  }
-  (void)lane;
-  wave_lds_sync();
   return NB;
 }
 
-// Writes the picked slots into W.nbr[0..count) (order: slot-major, then lane).
+// Inclusive prefix sum across the 64 lanes of a wave (DPP row shifts, then row
+// broadcasts to carry the row totals).
+__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x) {
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, true);  // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, true);  // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, true);  // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, true);  // row_shr:8
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xA, 0xF, false); // row_bcast:15
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xC, 0xF, false); // row_bcast:31
+  return x;
+}
+
+// Threshold selection of the closest 32 through a 64-bucket histogram of the
+// distance bits on [4, 8) (bucket = top six mantissa bits): one LDS atomic per
+// candidate, a wave prefix sum and one ballot locate the bucket of the 32nd
+// point; the bisection then only runs inside that bucket.  Same contract as
+// threshold32.
 template <int NS>
-__device__ __forceinline__ void compact(const uint32_t pick, const uint32_t (&key)[NS], const uint32_t (&lo)[NS],
-                                        const uint32_t (&hi)[NS], WaveLds& W) {
-  int base = 0;
+__device__ __forceinline__ int threshold32_hist(const uint32_t (&key)[NS], uint32_t* hist, int lane, uint32_t& thr,
+                                                uint32_t& tie_key, int& need, bool& suspect) {
+  const int clow = count_below(key, KEY_4);
+  if (clow >= NB) return threshold32<NS>(key, thr, tie_key, need, suspect);  // never expected
+  hist[lane] = 0;
+  wave_lds_sync();
 #pragma unroll
-  for (int s = 0; s < NS; ++s) {
-    const bool p = (pick >> s) & 1u;
-    const uint64_t m = __ballot(p);
-    if (p) {
-      Nbr& n = W.nbr[base + prefix_count(m)];
-      n.lo = lo[s];
-      n.hi = hi[s];
-      n.dbits = key[s];
-    }
-    base += __popcll(m);
+  for (int s = 0; s < NS; ++s)
+    if (key[s] >= KEY_4 && key[s] < KEY_8) atomicAdd(&hist[(key[s] - KEY_4) >> 17], 1u);
+  wave_lds_sync();
+  const uint32_t h = hist[lane];
+  const uint32_t pre = wave_inclusive_scan(h);
+  const int n8 = clow + (int)__builtin_amdgcn_readlane(pre, 63);
+  tie_key = KEY_INF;
+  need = 0;
+  if (n8 <= NB) {
+    thr = KEY_8;
+    suspect = true;
+    return n8;
   }
+  const uint64_t m = __ballot(clow + (int)pre >= NB);
+  const int b = (int)__builtin_ctzll(m);
+  const int below = clow + (int)__builtin_amdgcn_readlane(pre, b) - (int)__builtin_amdgcn_readlane(h, b);
+  const int inb = (int)__builtin_amdgcn_readlane(h, b);
+  uint32_t lo_k = KEY_4 + ((uint32_t)b << 17), hi_k = lo_k + (1u << 17);
+  if (below + inb == NB) {
+    thr = hi_k;
+    suspect = hi_k > KEY_SUSPECT;
+    return NB;
+  }
+  // invariant count(< lo) = below < 32 < count(< hi)
+  while (hi_k - lo_k > 1) {
+    const uint32_t mid = lo_k + ((hi_k - lo_k) >> 1);
+    const int c = count_below(key, mid);
+    if (c == NB) {
+      thr = mid;
+      suspect = mid > KEY_SUSPECT;
+      return NB;
+    }
+    if (c < NB)
+      lo_k = mid;
+    else
+      hi_k = mid;
+  }
+  thr = lo_k;
+  tie_key = lo_k;
+  need = NB - count_below(key, lo_k);
+  suspect = lo_k > KEY_SUSPECT;
+  return NB;
 }
 
 struct Search {
-  const Params& P;
   BlockLds& S;
   WaveLds& W;
-  int wave;
   int lane;
   uint32_t wbyte;
   uint32_t lo[NS_STRICT], hi[NS_STRICT];
-  bool ok[NS_STRICT];
   // lane constants of the table build: coordinate i = lane/8, value v = lane%8
-  int ti, tv, tK;
-  uint32_t tS;
+  int ti, tp, tK;
+  uint32_t tS, tN0;
   uint32_t toff;  // byte offset of entry (i, w, v)
 
-  __device__ Search(const Params& p, BlockLds& s, int w, int l)
-      : P(p), S(s), W(s.wave[w]), wave(w), lane(l), wbyte(64u * (uint32_t)w) {
+  // (the kernel argument is read field by field: holding a reference to it
+  // would force the argument block into private memory)
+  __device__ Search(const Params P, BlockLds& s, int w, int l)
+      : S(s), W(s.wave[w]), lane(l), wbyte(64u * (uint32_t)w) {
 #pragma unroll
-    for (int k = 0; k < NS_STRICT; ++k) ok[k] = load_candidate<0>(lane + WAVE * k, wbyte, lo[k], hi[k]);
+    for (int k = 0; k < NS_STRICT; ++k) load_candidate<0>(lane + WAVE * k, wbyte, lo[k], hi[k]);
     ti = lane >> 3;
-    tv = lane & 7;
-    tK = 0;
-    tS = 0;
+    tp = (lane & 7) + CMIN;
+    tK = P.K[0];
+    tS = P.S[0];
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      if (i == ti) {
-        tK = P.K[i];
-        tS = P.S[i];
-      }
-    toff = 256u * ti + wbyte + 4u * tv;
+    for (int i = 1; i < 8; ++i) {
+      tK = ti == i ? P.K[i] : tK;
+      tS = ti == i ? P.S[i] : tS;
+    }
+    tN0 = ti == 0 ? P.N : 0u;
+    toff = 256u * ti + wbyte + 4u * (lane & 7);
+  }
+
+  // Candidate (lo, hi) of lane-slot s: strict list in registers, boundary list
+  // (only needed on the rare path) from constant memory.
+  __device__ __forceinline__ void cand(int s, uint32_t& l, uint32_t& h) const {
+    if (s < NS_STRICT) {
+      l = lo[s];
+      h = hi[s];
+    } else {
+      load_candidate<1>(lane + WAVE * (s - NS_STRICT), wbyte, l, h);
+    }
   }
 
   // Per-query tables for frame F: entry (i, v) describes the lattice
   // coordinate k_i = c_i + s'_i (v + CMIN).
-  __device__ void build_tables(const Frame& F) {
+  __device__ __forceinline__ void build_tables(const Frame& F, uint32_t misc) {
     const float xi = F.x[ti];
     const int ci = F.c[ti];
-    const int p = tv + CMIN;
-    const int k = ((F.misc >> ti) & 1u) ? ci - p : ci + p;
+    const int k = ((misc >> ti) & 1u) ? ci - tp : ci + tp;
     const float e = xi - (float)k;
     const float e2 = e * e;
     const int par = k & 1;
     int Y = (k - par) >> 1;
-    // Y is within one period of [0, K) either side plus 3
-    while (Y < 0) Y += tK;
-    while (Y >= tK) Y -= tK;
-    const uint32_t sl = (uint32_t)Y * tS + ((ti == 0 && par) ? P.N : 0u);
+    // |x_i| < 2K, |x_i - c_i| <= 2 and |p| <= 4 put Y within [-K-3, K+3]: two
+    // periods up or one down wrap it for K >= 4, K = 2 is a parity; the clamp
+    // makes sure no rounding surprise can ever address outside the table
+    Y += Y < 0 ? tK : 0;
+    Y += Y < 0 ? tK : 0;
+    Y -= Y >= tK ? tK : 0;
+    Y = tK == 2 ? (Y & 1) : min(max(Y, 0), tK - 1);
+    const uint32_t sl = (uint32_t)Y * tS + (par ? tN0 : 0u);
     *reinterpret_cast<float*>(reinterpret_cast<char*>(S.qt) + toff) = e2;
     *reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(S.st) + toff) = sl;
     *reinterpret_cast<float*>(reinterpret_cast<char*>(S.et) + toff) = e;
   }
 
-  // Full neighbour search for frame F.  Leaves W.nbr[0..32) with
-  // (lo, hi, dbits, slot) and W.wgt with the fp32 recipe weights, padded with
-  // slot -1 / weight 0; returns the number of real neighbours.
-  __device__ int run(const Frame& F, uint32_t (&sel)[8]) {
-    const uint4* fs = reinterpret_cast<const uint4*>(F.sel);
-    const uint4 s0 = fs[0], s1 = fs[1];
-    sel[0] = s0.x; sel[1] = s0.y; sel[2] = s0.z; sel[3] = s0.w;
-    sel[4] = s1.x; sel[5] = s1.y; sel[6] = s1.z; sel[7] = s1.w;
+  // Writes the selected candidates into W.nbr[buf][0..count) (slot-major, then
+  // lane order); ties at the 32nd place are broken by (location, lattice point).
+  template <int NS>
+  __device__ __forceinline__ void emit(const uint32_t (&key)[NS], uint32_t thr, uint32_t tie_key, int need,
+                                       const Sel& sel, const Frame& F, int buf) {
+    int nt = 0;
+    if (tie_key != KEY_INF) {
+      // rare: list the tied candidates' (location, lattice point) keys (unrolled:
+      // a runtime index into the candidate registers would spill them)
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        const bool tied = key[s] == tie_key;
+        const uint64_t m = __ballot(tied);
+        if (m) {
+          uint32_t l, h;
+          cand(s, l, h);
+          const int pos = nt + prefix_count(m);
+          if (tied && pos < TIE_MAX) {
+            W.tie[pos][0] = (uint32_t)cand_slot(S.st, l, h, sel);
+            W.tie[pos][1] = cand_liftkey(l, h, sel, F);
+          }
+          nt += __popcll(m);
+        }
+      }
+      nt = min(nt, TIE_MAX);
+      wave_lds_sync();
+    }
+    int base = 0;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      bool p = key[s] < thr;
+      if (tie_key != KEY_INF && key[s] == tie_key) {
+        uint32_t l, h;
+        cand(s, l, h);
+        const uint32_t ms = (uint32_t)cand_slot(S.st, l, h, sel);
+        const uint32_t mk = cand_liftkey(l, h, sel, F);
+        int rank = 0;
+#pragma unroll 1
+        for (int e = 0; e < nt; ++e) {
+          const uint32_t es = W.tie[e][0], ek = W.tie[e][1];
+          rank += (es < ms || (es == ms && ek < mk)) ? 1 : 0;
+        }
+        p = rank < need;
+      }
+      const uint64_t m = __ballot(p);
+      if (p) {
+        uint32_t l, h;
+        cand(s, l, h);
+        Nbr& n = W.nbr[buf][base + prefix_count(m)];
+        n.lo = l;
+        n.hi = h;
+        n.dbits = key[s];
+      }
+      base += __popcll(m);
+    }
+  }
+
+  // Full neighbour search of frame F into buffer `buf`: W.nbr[buf][0..32) with
+  // (lo, hi, dbits, slot) and W.wgt[buf] with the fp32 recipe weights, padded
+  // with slot -1 / weight 0.  Returns the number of real neighbours.
+  __device__ int run(const Frame& F, const Sel& sel, int buf) {
     int count = 0;
-    if (F.misc & 0x100u) {
-      build_tables(F);
+    if (sel.misc & 0x100u) {
+      build_tables(F, sel.misc);
       wave_lds_sync();
       uint32_t key[NS_STRICT];
 #pragma unroll
       for (int k = 0; k < NS_STRICT; ++k)
-        key[k] = ok[k] ? __float_as_uint(cand_d2(S.qt, lo[k], hi[k], sel)) : KEY_INF;
-      uint32_t pick;
+        key[k] = (lane + WAVE * k < E8_NSTRICT) ? __float_as_uint(cand_d2(S.qt, lo[k], hi[k], sel)) : KEY_INF;
+      uint32_t thr, tie_key;
+      int need;
       bool suspect;
-      count = select32<NS_STRICT>(key, lo, hi, sel, F, S.st, W, pick, suspect);
+      count = threshold32_hist<NS_STRICT>(key, W.hist, lane, thr, tie_key, need, suspect);
       if (!suspect) {
-        compact<NS_STRICT>(pick, key, lo, hi, W);
+        emit<NS_STRICT>(key, thr, tie_key, need, sel, F, buf);
       } else {
         // rare: rescan together with the points at distance exactly sqrt(8) from F
-        uint32_t key7[NS_ALL], lo7[NS_ALL], hi7[NS_ALL];
+        uint32_t key7[NS_ALL];
 #pragma unroll
-        for (int k = 0; k < NS_STRICT; ++k) {
-          key7[k] = key[k];
-          lo7[k] = lo[k];
-          hi7[k] = hi[k];
-        }
-#pragma unroll
+        for (int k = 0; k < NS_STRICT; ++k) key7[k] = key[k];
+#pragma unroll 1
         for (int k = 0; k < NS_BOUND; ++k) {
-          const bool okb = load_candidate<1>(lane + WAVE * k, wbyte, lo7[NS_STRICT + k], hi7[NS_STRICT + k]);
-          key7[NS_STRICT + k] =
-              okb ? __float_as_uint(cand_d2(S.qt, lo7[NS_STRICT + k], hi7[NS_STRICT + k], sel)) : KEY_INF;
+          uint32_t l, h;
+          const bool okb = load_candidate<1>(lane + WAVE * k, wbyte, l, h);
+          key7[NS_STRICT + k] = okb ? __float_as_uint(cand_d2(S.qt, l, h, sel)) : KEY_INF;
         }
         bool suspect7;
-        count = select32<NS_ALL>(key7, lo7, hi7, sel, F, S.st, W, pick, suspect7);
-        compact<NS_ALL>(pick, key7, lo7, hi7, W);
+        count = threshold32<NS_ALL>(key7, thr, tie_key, need, suspect7);
+        emit<NS_ALL>(key7, thr, tie_key, need, sel, F, buf);
       }
       wave_lds_sync();
     }
     // locations and weights, one neighbour per lane
     if (lane < NB) {
-      Nbr& n = W.nbr[lane];
+      Nbr& n = W.nbr[buf][lane];
       if (lane < count) {
         n.slot = cand_slot(S.st, n.lo, n.hi, sel);
-        const float d = __uint_as_float(n.dbits);
-        const float u = 1.0f - d * 0.125f;
+        const float u = 1.0f - __uint_as_float(n.dbits) * 0.125f;
         const float u2 = u * u;
-        W.wgt[lane] = u2 * u2;
+        W.wgt[buf][lane] = u2 * u2;
       } else {
         n.lo = n.hi = 0;
         n.dbits = KEY_INF;
         n.slot = -1;
-        W.wgt[lane] = 0.0f;
+        W.wgt[buf][lane] = 0.0f;
       }
     }
     wave_lds_sync();
@@ -514,50 +606,61 @@ struct Search {
   }
 };
 
-// Phase A for the wave's 64 lookups starting at `base`.
-__device__ __forceinline__ void phase_a(const float* __restrict__ q, int64_t base, const Params& P, WaveLds& W,
-                                        int lane) {
-  const int64_t l = base + lane;
-  const bool have = l < P.L;
-  make_frame(q + (have ? l : 0) * 8, have, P, W.frames[lane]);
+// Phase A for the wave's lookups [base, base + lpw).
+__device__ __forceinline__ void phase_a(const float* __restrict__ q, int64_t base, int nl, const Params P,
+                                        WaveLds& W, int lane) {
+  if (lane < nl) make_frame(q + (base + lane) * 8, true, P, W.frames[lane]);
   wave_lds_sync();
 }
 
 // ---------------------------------------------------------------------------
 // Kernels.
 
+struct WaveCtx {
+  int wave, lane;
+  int64_t base;
+  int nl;
+};
+
+__device__ __forceinline__ bool wave_ctx(const Params P, WaveCtx& c) {
+  c.wave = threadIdx.x / WAVE;
+  c.lane = threadIdx.x % WAVE;
+  c.base = ((int64_t)blockIdx.x * WAVES + c.wave) * P.lpw;
+  if (c.base >= P.L) return false;
+  c.nl = (int)min<int64_t>(P.lpw, P.L - c.base);
+  return true;
+}
+
 __global__ void __launch_bounds__(THREADS) k_neighbors(const float* __restrict__ q, Params P,
                                                        int32_t* __restrict__ slot_out, float* __restrict__ w_out,
                                                        float* __restrict__ d2_out) {
   __shared__ BlockLds S;
-  const int wave = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
-  const int64_t base = ((int64_t)blockIdx.x * WAVES + wave) * WAVE;
-  if (base >= P.L) return;
-  Search srch(P, S, wave, lane);
-  WaveLds& W = S.wave[wave];
-  phase_a(q, base, P, W, lane);
-  const int nl = (int)min<int64_t>(WAVE, P.L - base);
-  for (int t = 0; t < nl; ++t) {
-    uint32_t sel[8];
+  WaveCtx c;
+  if (!wave_ctx(P, c)) return;
+  Search srch(P, S, c.wave, c.lane);
+  WaveLds& W = S.wave[c.wave];
+  phase_a(q, c.base, c.nl, P, W, c.lane);
+  for (int t = 0; t < c.nl; ++t) {
     const Frame& F = W.frames[t];
-    const int count = srch.run(F, sel);
-    const int64_t l = base + t;
-    if (lane < NB) {
+    const Sel sel = read_sel(F);
+    const int count = srch.run(F, sel, 0);
+    const int64_t l = c.base + t;
+    if (c.lane < NB) {
       // order the list by (distance bits, location, lattice point)
-      const Nbr me = W.nbr[lane];
-      int rank = lane;
-      if (lane < count) {
+      const Nbr me = W.nbr[0][c.lane];
+      int rank = c.lane;
+      if (c.lane < count) {
         const uint32_t mk = cand_liftkey(me.lo, me.hi, sel, F);
         rank = 0;
         for (int e = 0; e < count; ++e) {
-          const Nbr o = W.nbr[e];
+          const Nbr o = W.nbr[0][e];
           bool less = o.dbits < me.dbits || (o.dbits == me.dbits && o.slot < me.slot);
-          if (o.dbits == me.dbits && o.slot == me.slot && e != lane) less = cand_liftkey(o.lo, o.hi, sel, F) < mk;
+          if (o.dbits == me.dbits && o.slot == me.slot && e != c.lane) less = cand_liftkey(o.lo, o.hi, sel, F) < mk;
           rank += less ? 1 : 0;
         }
       }
       slot_out[l * NB + rank] = me.slot;
-      w_out[l * NB + rank] = W.wgt[lane];
+      w_out[l * NB + rank] = W.wgt[0][c.lane];
       if (d2_out) d2_out[l * NB + rank] = __uint_as_float(me.dbits);
     }
     wave_lds_sync();
@@ -590,61 +693,102 @@ __device__ __forceinline__ void unpack16(const uint4 v, float (&f)[EPC]) {
   }
 }
 
+// Gather geometry of the forward: each lane reads BPL contiguous bytes of a row,
+// LPR lanes cover a row, one load instruction covers RPI rows, NI instructions
+// cover the 32 rows; a lane accumulates EPL output elements over its NI rows and
+// the RPI row groups are summed with xor shuffles.
+template <int DT, int M>
+struct FwdGeom {
+  static constexpr int ES = DT == LRAM_F32 ? 4 : 2;
+  static constexpr int RB = M * ES;
+  static constexpr int BPL = (DT == LRAM_F32 && M == 64) ? 8 : 4;
+  static constexpr int LPR = RB / BPL;
+  static constexpr int RPI = WAVE / LPR;
+  static constexpr int NI = NB / RPI;
+  static constexpr int EPL = BPL / ES;
+  static constexpr int DW = BPL / 4;  // dwords per lane per row
+  static_assert(LPR <= WAVE && WAVE % LPR == 0 && NB % RPI == 0, "forward gather geometry");
+};
+
+template <int DT, int M>
+__device__ __forceinline__ void fwd_issue(const char* __restrict__ tb, const WaveLds& W, int buf, int lane,
+                                          uint32_t (&v)[FwdGeom<DT, M>::NI][FwdGeom<DT, M>::DW]) {
+  using G = FwdGeom<DT, M>;
+  const int rsub = lane / G::LPR, col = lane % G::LPR;
+#pragma unroll
+  for (int p = 0; p < G::NI; ++p) {
+    const int32_t s = W.nbr[buf][p * G::RPI + rsub].slot;
+    const char* src = tb + (size_t)(s >= 0 ? s : 0) * G::RB + col * G::BPL;
+    if constexpr (G::DW == 1) {
+      v[p][0] = s >= 0 ? *reinterpret_cast<const uint32_t*>(src) : 0u;
+    } else {
+      const uint2 t = s >= 0 ? *reinterpret_cast<const uint2*>(src) : make_uint2(0, 0);
+      v[p][0] = t.x;
+      v[p][1] = t.y;
+    }
+  }
+}
+
+template <int DT, int M>
+__device__ __forceinline__ void fwd_consume(const WaveLds& W, int buf, int lane, int64_t l,
+                                            const uint32_t (&v)[FwdGeom<DT, M>::NI][FwdGeom<DT, M>::DW],
+                                            void* __restrict__ out) {
+  using G = FwdGeom<DT, M>;
+  const int rsub = lane / G::LPR, col = lane % G::LPR;
+  float acc[G::EPL];
+#pragma unroll
+  for (int e = 0; e < G::EPL; ++e) acc[e] = 0.0f;
+#pragma unroll
+  for (int p = 0; p < G::NI; ++p) {
+    const float w = W.wgt[buf][p * G::RPI + rsub];
+    if constexpr (DT == LRAM_F32) {
+#pragma unroll
+      for (int e = 0; e < G::EPL; ++e) acc[e] = fmaf(w, __uint_as_float(v[p][e]), acc[e]);
+    } else {
+#pragma unroll
+      for (int d = 0; d < G::DW; ++d) {
+        acc[2 * d] = fmaf(w, bf16_lo(v[p][d]), acc[2 * d]);
+        acc[2 * d + 1] = fmaf(w, bf16_hi(v[p][d]), acc[2 * d + 1]);
+      }
+    }
+  }
+#pragma unroll
+  for (int mask = G::LPR; mask < WAVE; mask <<= 1)
+#pragma unroll
+    for (int e = 0; e < G::EPL; ++e) acc[e] += __shfl_xor(acc[e], mask);
+  if (rsub == 0) {
+    char* ob = reinterpret_cast<char*>(out) + (size_t)l * G::RB + col * G::BPL;
+    if constexpr (DT == LRAM_F32) {
+      if constexpr (G::EPL == 1)
+        *reinterpret_cast<float*>(ob) = acc[0];
+      else
+        *reinterpret_cast<float2*>(ob) = make_float2(acc[0], acc[1]);
+    } else {
+      *reinterpret_cast<uint32_t*>(ob) = pack_bf16x2(acc[0], acc[1]);
+    }
+  }
+}
+
 template <int DT, int M>
 __global__ void __launch_bounds__(THREADS) k_forward(const float* __restrict__ q, Params P,
                                                      const void* __restrict__ table, void* __restrict__ out) {
-  using G = RowGeom<DT, M>;
+  using G = FwdGeom<DT, M>;
   __shared__ BlockLds S;
-  const int wave = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
-  const int64_t base = ((int64_t)blockIdx.x * WAVES + wave) * WAVE;
-  if (base >= P.L) return;
-  Search srch(P, S, wave, lane);
-  WaveLds& W = S.wave[wave];
-  phase_a(q, base, P, W, lane);
-  const int nl = (int)min<int64_t>(WAVE, P.L - base);
-  const int rsub = lane / G::LPR, ch = lane % G::LPR;
+  WaveCtx c;
+  if (!wave_ctx(P, c)) return;
+  Search srch(P, S, c.wave, c.lane);
+  WaveLds& W = S.wave[c.wave];
+  phase_a(q, c.base, c.nl, P, W, c.lane);
   const char* tb = reinterpret_cast<const char*>(table);
-  for (int t = 0; t < nl; ++t) {
-    uint32_t sel[8];
-    srch.run(W.frames[t], sel);
-    uint4 v[G::NP];
-    float w[G::NP];
-#pragma unroll
-    for (int p = 0; p < G::NP; ++p) {
-      const int j = p * G::RPP + rsub;
-      const int32_t s = W.nbr[j].slot;
-      w[p] = W.wgt[j];
-      v[p] = s >= 0 ? *reinterpret_cast<const uint4*>(tb + (size_t)s * G::RB + ch * 16) : make_uint4(0, 0, 0, 0);
-    }
-    float acc[G::EPC];
-#pragma unroll
-    for (int e = 0; e < G::EPC; ++e) acc[e] = 0.0f;
-#pragma unroll
-    for (int p = 0; p < G::NP; ++p) {
-      float f[G::EPC];
-      unpack16<DT, G::EPC>(v[p], f);
-#pragma unroll
-      for (int e = 0; e < G::EPC; ++e) acc[e] = fmaf(w[p], f[e], acc[e]);
-    }
-#pragma unroll
-    for (int mask = G::LPR; mask < WAVE; mask <<= 1)
-#pragma unroll
-      for (int e = 0; e < G::EPC; ++e) acc[e] += __shfl_xor(acc[e], mask);
-    if (rsub == 0) {
-      const int64_t l = base + t;
-      char* ob = reinterpret_cast<char*>(out) + (size_t)l * G::RB + ch * 16;
-      if constexpr (DT == LRAM_F32) {
-        *reinterpret_cast<float4*>(ob) = make_float4(acc[0], acc[1], acc[2], acc[3]);
-      } else {
-        uint4 o;
-        o.x = f32_to_bf16_rne(acc[0]) | (f32_to_bf16_rne(acc[1]) << 16);
-        o.y = f32_to_bf16_rne(acc[2]) | (f32_to_bf16_rne(acc[3]) << 16);
-        o.z = f32_to_bf16_rne(acc[4]) | (f32_to_bf16_rne(acc[5]) << 16);
-        o.w = f32_to_bf16_rne(acc[6]) | (f32_to_bf16_rne(acc[7]) << 16);
-        *reinterpret_cast<uint4*>(ob) = o;
-      }
-    }
-    wave_lds_sync();
+  uint32_t v[G::NI][G::DW];
+  srch.run(W.frames[0], read_sel(W.frames[0]), 0);
+  fwd_issue<DT, M>(tb, W, 0, c.lane, v);
+  for (int t = 0; t < c.nl; ++t) {
+    const int buf = t & 1;
+    // search lookup t+1 while the rows of lookup t are in flight
+    if (t + 1 < c.nl) srch.run(W.frames[t + 1], read_sel(W.frames[t + 1]), buf ^ 1);
+    fwd_consume<DT, M>(W, buf, c.lane, c.base + t, v, out);
+    if (t + 1 < c.nl) fwd_issue<DT, M>(tb, W, buf ^ 1, c.lane, v);
   }
 }
 
@@ -662,33 +806,25 @@ __global__ void __launch_bounds__(THREADS) k_backward(const float* __restrict__ 
   using G = RowGeom<DT, M>;
   constexpr int ICOORD = G::LPR >= 8 ? 1 : 8 / G::LPR;  // query coordinates per lane
   __shared__ BlockLds S;
-  const int wave = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
-  const int64_t base = ((int64_t)blockIdx.x * WAVES + wave) * WAVE;
-  if (base >= P.L) return;
-  Search srch(P, S, wave, lane);
-  WaveLds& W = S.wave[wave];
-  phase_a(q, base, P, W, lane);
-  const int nl = (int)min<int64_t>(WAVE, P.L - base);
+  WaveCtx c;
+  if (!wave_ctx(P, c)) return;
+  const int lane = c.lane;
+  Search srch(P, S, c.wave, lane);
+  WaveLds& W = S.wave[c.wave];
+  phase_a(q, c.base, c.nl, P, W, lane);
   const int rsub = lane / G::LPR, ch = lane % G::LPR;
   const char* tb = reinterpret_cast<const char*>(table);
-  for (int t = 0; t < nl; ++t) {
-    uint32_t sel[8];
+  for (int t = 0; t < c.nl; ++t) {
     const Frame& F = W.frames[t];
-    const int count = srch.run(F, sel);
-    const int64_t l = base + t;
+    const Sel sel = read_sel(F);
+    const int count = srch.run(F, sel, 0);
+    const int64_t l = c.base + t;
     float dq[ICOORD];
 #pragma unroll
-    for (int c = 0; c < ICOORD; ++c) dq[c] = 0.0f;
+    for (int k = 0; k < ICOORD; ++k) dq[k] = 0.0f;
     if (count > 0) {
-      float g[G::EPC];
-      const float* gp = gout + (size_t)l * M + ch * G::EPC;
-#pragma unroll
-      for (int e = 0; e < G::EPC; e += 4) {
-        const float4 gv = *reinterpret_cast<const float4*>(gp + e);
-        g[e] = gv.x; g[e + 1] = gv.y; g[e + 2] = gv.z; g[e + 3] = gv.w;
-      }
       // value-gradient scatter: M consecutive lanes own one gradient row, so each
-      // atomic instruction covers 64/M whole rows (full-line requests at L2)
+      // atomic instruction covers 64/M whole rows
       if (!EMIT && gtab) {
         constexpr int RA = WAVE / M;
         const int col = lane % M;
@@ -696,60 +832,74 @@ __global__ void __launch_bounds__(THREADS) k_backward(const float* __restrict__ 
 #pragma unroll 4
         for (int k = 0; k < NB / RA; ++k) {
           const int j = k * RA + lane / M;
-          const int32_t s = W.nbr[j].slot;
-          if (s >= 0) unsafeAtomicAdd(gtab + (size_t)s * M + col, W.wgt[j] * gc);
+          const int32_t s = W.nbr[0][j].slot;
+          if (s >= 0) unsafeAtomicAdd(gtab + (size_t)s * M + col, W.wgt[0][j] * gc);
         }
       }
-      uint4 v[G::NP];
-      int32_t sl[G::NP];
+      if (gq) {
+        float g[G::EPC];
+        const float* gp = gout + (size_t)l * M + ch * G::EPC;
 #pragma unroll
-      for (int p = 0; p < G::NP; ++p) {
-        const int j = p * G::RPP + rsub;
-        sl[p] = W.nbr[j].slot;
-        v[p] = sl[p] >= 0 ? *reinterpret_cast<const uint4*>(tb + (size_t)sl[p] * G::RB + ch * 16)
-                          : make_uint4(0, 0, 0, 0);
-      }
+        for (int e = 0; e < G::EPC; e += 4) {
+          const float4 gv = *reinterpret_cast<const float4*>(gp + e);
+          g[e] = gv.x; g[e + 1] = gv.y; g[e + 2] = gv.z; g[e + 3] = gv.w;
+        }
+        // per-lane selectors of the query coordinates this lane accumulates
+        uint32_t lsel[ICOORD];
 #pragma unroll
-      for (int p = 0; p < G::NP; ++p) {
-        const int j = p * G::RPP + rsub;
-        float f[G::EPC];
-        unpack16<DT, G::EPC>(v[p], f);
-        float pd = 0.0f;
+        for (int k = 0; k < ICOORD; ++k) {
+          lsel[k] = F.sel[(ch + k * G::LPR) & 7];
+        }
+        uint4 v[G::NP];
+        int32_t sl[G::NP];
 #pragma unroll
-        for (int e = 0; e < G::EPC; ++e) pd = fmaf(g[e], f[e], pd);
-        // <G, v_j>: sum over the LPR lanes of this row
+        for (int p = 0; p < G::NP; ++p) {
+          sl[p] = W.nbr[0][p * G::RPP + rsub].slot;
+          v[p] = sl[p] >= 0 ? *reinterpret_cast<const uint4*>(tb + (size_t)sl[p] * G::RB + ch * 16)
+                            : make_uint4(0, 0, 0, 0);
+        }
 #pragma unroll
-        for (int mask = 1; mask < G::LPR; mask <<= 1) pd += __shfl_xor(pd, mask);
-        if (gq && sl[p] >= 0) {
-          const Nbr n = W.nbr[j];
-          const float u = 1.0f - __uint_as_float(n.dbits) * 0.125f;
-          const float a = -2.0f * u * u * u * pd;
+        for (int p = 0; p < G::NP; ++p) {
+          const int j = p * G::RPP + rsub;
+          float f[G::EPC];
+          unpack16<DT, G::EPC>(v[p], f);
+          float pd = 0.0f;
 #pragma unroll
-          for (int c = 0; c < ICOORD; ++c) {
-            const int i = ch + c * G::LPR;
-            if (i < 8) {
-              const uint32_t ab = __builtin_amdgcn_perm(n.hi, n.lo, F.sel[i]);
-              dq[c] = fmaf(a, lds_f32(S.et, ab + 256u * i), dq[c]);
+          for (int e = 0; e < G::EPC; ++e) pd = fmaf(g[e], f[e], pd);
+          // <G, v_j>: sum over the LPR lanes of this row
+#pragma unroll
+          for (int mask = 1; mask < G::LPR; mask <<= 1) pd += __shfl_xor(pd, mask);
+          if (sl[p] >= 0) {
+            const Nbr n = W.nbr[0][j];
+            const float u = 1.0f - __uint_as_float(n.dbits) * 0.125f;
+            const float a = -2.0f * u * u * u * pd;
+#pragma unroll
+            for (int k = 0; k < ICOORD; ++k) {
+              const int i = ch + k * G::LPR;
+              if (i < 8) {
+                const uint32_t ab = __builtin_amdgcn_perm(n.hi, n.lo, lsel[k]);
+                dq[k] = fmaf(a, lds_f32(S.et, ab + 256u * i), dq[k]);
+              }
             }
           }
         }
       }
     }
     if (EMIT && gtab && lane < NB) {
-      const int32_t sl = W.nbr[lane].slot;
-      pair_key[l * NB + lane] = sl >= 0 ? (uint32_t)sl : P.N;
-      pair_val[l * NB + lane] = make_uint2((uint32_t)l, __float_as_uint(W.wgt[lane]));
+      const int32_t s = W.nbr[0][lane].slot;
+      pair_key[l * NB + lane] = s >= 0 ? (uint32_t)s : P.N;
+      pair_val[l * NB + lane] = make_uint2((uint32_t)l, __float_as_uint(W.wgt[0][lane]));
     }
     if (gq) {
 #pragma unroll
       for (int mask = G::LPR; mask < WAVE; mask <<= 1)
 #pragma unroll
-        for (int c = 0; c < ICOORD; ++c) dq[c] += __shfl_xor(dq[c], mask);
+        for (int k = 0; k < ICOORD; ++k) dq[k] += __shfl_xor(dq[k], mask);
       if (rsub == 0) {
 #pragma unroll
-        for (int c = 0; c < ICOORD; ++c) {
-          const int i = ch + c * G::LPR;
-          if (i < 8) gq[l * 8 + i] = dq[c];
+        for (int k = 0; k < ICOORD; ++k) {
+          const int i = ch + k * G::LPR;
+          if (i < 8) gq[l * 8 + i] = dq[k];
         }
       }
     }
@@ -757,8 +907,6 @@ __global__ void __launch_bounds__(THREADS) k_backward(const float* __restrict__ 
   }
 }
 
-
-// ---------------------------------------------------------------------------
 // Sorted value-gradient scatter: a stable LSD radix sort of the (location,
 // (lookup, weight)) pairs by location, then a segmented reduction that writes
 // every touched gradient row with one read-modify-write.
@@ -996,7 +1144,7 @@ int check_common(const float* q, int64_t B, int64_t H, const int32_t* K, int64_t
   *L = B * H;
   int64_t N = 1;
   for (int i = 0; i < 8; ++i) {
-    if (K[i] < 2 || (K[i] & 1)) return LRAM_EBADK;
+    if (K[i] < 2 || (K[i] & 1) || K[i] > KMAX) return LRAM_EBADK;
     N *= K[i];
     if (N >= (int64_t(1) << 31)) return LRAM_EBADK;
   }
@@ -1012,6 +1160,11 @@ int check_common(const float* q, int64_t B, int64_t H, const int32_t* K, int64_t
   }
   P->N = (uint32_t)N;
   P->L = *L;
+  // lookups per wave: up to 64, fewer for small batches so that every CU gets
+  // work (about 16 waves per CU for 256 CUs)
+  const int64_t target_waves = 256 * 16;
+  int64_t lpw = (*L + target_waves - 1) / target_waves;
+  P->lpw = (int32_t)(lpw < 1 ? 1 : (lpw > WAVE ? WAVE : lpw));
   return LRAM_OK;
 }
 
@@ -1032,7 +1185,10 @@ int launched() {
   return LRAM_OK;
 }
 
-unsigned grid_for(int64_t L) { return (unsigned)((L + THREADS - 1) / THREADS); }
+unsigned grid_for(const Params& P) {
+  const int64_t per_block = (int64_t)P.lpw * WAVES;
+  return (unsigned)((P.L + per_block - 1) / per_block);
+}
 
 template <template <int, int> class Launcher, typename... Args>
 int dispatch(int dtype, int32_t m, Args... args) {
@@ -1046,7 +1202,7 @@ int dispatch(int dtype, int32_t m, Args... args) {
 template <int DT, int M>
 struct FwdLaunch {
   static int go(const float* q, const Params& P, const void* table, void* out, hipStream_t s) {
-    hipLaunchKernelGGL((k_forward<DT, M>), dim3(grid_for(P.L)), dim3(THREADS), 0, s, q, P, table, out);
+    hipLaunchKernelGGL((k_forward<DT, M>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, out);
     return launched();
   }
 };
@@ -1091,7 +1247,7 @@ template <int DT, int M>
 struct BwdAtomicLaunch {
   static int go(const float* q, const Params& P, const void* table, const float* g, float* gt, float* gq,
                 hipStream_t s) {
-    hipLaunchKernelGGL((k_backward<DT, M, false>), dim3(grid_for(P.L)), dim3(THREADS), 0, s, q, P, table, g,
+    hipLaunchKernelGGL((k_backward<DT, M, false>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g,
                        gt, gq, (uint32_t*)nullptr, (uint2*)nullptr);
     return launched();
   }
@@ -1101,7 +1257,7 @@ template <int DT, int M>
 struct BwdSortedLaunch {
   static int go(const float* q, const Params& P, const void* table, const float* g, float* gt, float* gq,
                 const SortWs& ws, hipStream_t s) {
-    hipLaunchKernelGGL((k_backward<DT, M, true>), dim3(grid_for(P.L)), dim3(THREADS), 0, s, q, P, table, g, gt,
+    hipLaunchKernelGGL((k_backward<DT, M, true>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g, gt,
                        gq, ws.k0, ws.v0);
     int rc = launched();
     if (rc || !gt) return rc;
@@ -1159,7 +1315,7 @@ int lram_neighbors(const float* q, int64_t B, int64_t H, const int32_t K[8], int
   if (rc) return rc;
   if (L == 0) return LRAM_OK;
   if (!slot || !w) return LRAM_EINVAL;
-  hipLaunchKernelGGL(k_neighbors, dim3(grid_for(L)), dim3(THREADS), 0, (hipStream_t)stream, q, P, slot, w, d2);
+  hipLaunchKernelGGL(k_neighbors, dim3(grid_for(P)), dim3(THREADS), 0, (hipStream_t)stream, q, P, slot, w, d2);
   return launched();
 }
 
