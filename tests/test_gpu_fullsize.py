@@ -1,0 +1,132 @@
+"""Parity at full size, in the launch configuration the benchmark times.
+
+For the three large workloads the whole batch runs through lram_neighbors,
+lram_forward and lram_backward exactly as bench.py calls them; the oracle then
+checks sampled outputs one by one:
+  * neighbour lists of sampled lookups: bit-exact;
+  * out and dq of sampled lookups: per-row relative L2 <= 1e-5 (fp32 table) or
+    <= 2e-2 (bf16 table), dq <= 1e-4 (fp32 kernel arithmetic vs fp64);
+  * gradient rows of sampled locations: the oracle accumulates the contribution
+    of every lookup of the batch (in chunks) to those rows; per-row relative L2
+    <= 1e-4 (fp32 atomics in any order vs fp64, up to ~3e4 terms per hot row);
+  * sampled locations no lookup touches: exactly 0.
+"""
+import gc
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2107_03474_amd as lram
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+def _rel_rows(a, b):
+    a = np.asarray(a, np.float64).reshape(a.shape[0], -1)
+    b = np.asarray(b, np.float64).reshape(b.shape[0], -1)
+    num = np.linalg.norm(a - b, axis=1)
+    den = np.linalg.norm(b, axis=1)
+    return np.where(den > 0, num / np.where(den > 0, den, 1), num)
+
+
+def _fits(w):
+    free, _ = torch.cuda.mem_get_info()
+    need = w.table_bytes + (w.N * w.m * 4 if w.backward else 0) + w.L * (32 * 12 + 4 * w.m + 64) + (4 << 30)
+    return need <= free, need, free
+
+
+def _rows(table, slots):
+    s = torch.from_numpy(np.asarray(slots, np.int64)).to(DEV)
+    r = table[s.clamp(min=0)].float()
+    r[s < 0] = 0
+    return r.cpu().numpy().astype(np.float64)
+
+
+@pytest.mark.parametrize("name", ["k8-m64-f32-uniform", "k12-m64-bf16-proj", "k14-m32-bf16-zipf"])
+def test_full_size(name):
+    w = W.WORKLOADS[name]
+    gc.collect()
+    torch.cuda.empty_cache()
+    ok, need, free = _fits(w)
+    if not ok:
+        pytest.skip("needs %.1f GB of device memory, %.1f GB free" % (need / 1e9, free / 1e9))
+    _say("full size", name, "- building inputs")
+    q_np = W.queries(w)
+    q = torch.from_numpy(q_np).to(DEV)
+    table = W.make_table(w, DEV)
+    out = torch.empty((w.B, w.H, w.m), dtype=table.dtype, device=DEV)
+    lram.forward(q, table, w.K, out=out)
+    slot, wgt, d2 = lram.neighbors(q, w.K)
+    if w.backward:
+        G = W.grad_out(w, DEV)
+        gtab = torch.zeros((w.N, w.m), dtype=torch.float32, device=DEV)
+        gq = torch.empty((w.B, w.H, 8), dtype=torch.float32, device=DEV)
+        lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq)
+    torch.cuda.synchronize()
+    _say("kernels done")
+
+    rng = np.random.default_rng(2024)
+    qf = q_np.reshape(-1, 8)
+    idx = np.sort(rng.choice(w.L, 4096, replace=False))
+    nb = oracle.neighbors(qf[idx], w.K)
+    np.testing.assert_array_equal(slot.reshape(-1, 32)[torch.from_numpy(idx).to(DEV)].cpu().numpy(), nb["slot"])
+    np.testing.assert_array_equal(d2.reshape(-1, 32)[torch.from_numpy(idx).to(DEV)].cpu().numpy().view(np.uint32),
+                                  nb["d2"].view(np.uint32))
+    rows = _rows(table, nb["slot"])
+    ref = oracle.forward(nb, rows)
+    got = out.reshape(-1, w.m)[torch.from_numpy(idx).to(DEV)].float().cpu().numpy()
+    tol = 1e-5 if w.dtype == "f32" else 2e-2
+    err = _rel_rows(got, ref)
+    _say("out: max rel err %.2e over %d sampled lookups" % (err.max(), idx.size))
+    assert err.max() <= tol
+    if not w.backward:
+        return
+    Gf = G.reshape(-1, w.m)
+    g_s = Gf[torch.from_numpy(idx).to(DEV)].cpu().numpy().astype(np.float64)
+    dq_ref = oracle.grad_query(nb, rows, g_s)
+    dq = gq.reshape(-1, 8)[torch.from_numpy(idx).to(DEV)].cpu().numpy()
+    err = _rel_rows(dq, dq_ref)
+    _say("dq: max rel err %.2e" % err.max())
+    assert err.max() <= (1e-4 if w.dtype == "f32" else 2e-2)
+
+    # gradient rows: sample touched locations, accumulate every lookup's part in fp64
+    touched = np.unique(nb["slot"][nb["slot"] >= 0])
+    pick = np.sort(rng.choice(touched, min(1024, touched.size), replace=False))
+    acc = np.zeros((pick.size, w.m), np.float64)
+    G_host = Gf.cpu().numpy()
+    chunk = 1 << 18
+    for s0 in range(0, w.L, chunk):
+        s1 = min(w.L, s0 + chunk)
+        nbc = oracle.neighbors(qf[s0:s1], w.K)
+        sl = nbc["slot"]
+        hit = np.isin(sl, pick)
+        if hit.any():
+            li, ji = np.nonzero(hit)
+            pos = np.searchsorted(pick, sl[li, ji])
+            np.add.at(acc, pos, nbc["w64"][li, ji][:, None] * G_host[s0 + li].astype(np.float64))
+        del nbc
+        gc.collect()
+        _say("oracle gradient rows: %d / %d lookups" % (s1, w.L))
+    got = gtab[torch.from_numpy(pick).to(DEV)].cpu().numpy()
+    err = _rel_rows(got, acc)
+    _say("dV: max rel err %.2e over %d sampled rows" % (err.max(), pick.size))
+    assert err.max() <= 1e-4
+    # locations nobody touched stay exactly zero
+    all_touched = torch.zeros(w.N, dtype=torch.bool, device=DEV)
+    sv = slot.reshape(-1)
+    all_touched[sv[sv >= 0].long()] = True
+    cand = torch.from_numpy(rng.choice(w.N, 4096, replace=False)).to(DEV)
+    cold = cand[~all_touched[cand]]
+    assert cold.numel() > 100
+    assert torch.count_nonzero(gtab[cold]).item() == 0
+    del table, gtab, G, out, slot, wgt, d2, all_touched
+    gc.collect()
+    torch.cuda.empty_cache()
