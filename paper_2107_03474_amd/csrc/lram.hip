@@ -1002,26 +1002,50 @@ __global__ void __launch_bounds__(THREADS) k_scan_add(uint32_t* __restrict__ a, 
 // Stable scatter of one radix pass.  Element order inside a tile is (round,
 // wave, lane), i.e. index order; ranks among equal digits come from an 8-ballot
 // match inside the wave plus per-(wave, digit) counts carried across rounds.
+// The tile is first ordered by digit in LDS (a 2-byte permutation), then
+// written out in that order so that consecutive threads store consecutive
+// addresses of a digit's output run.
 __global__ void __launch_bounds__(THREADS) k_radix_scatter(const uint32_t* __restrict__ kin,
                                                            const uint2* __restrict__ vin, int64_t n, int shift,
                                                            const uint32_t* __restrict__ offs, int nblocks,
                                                            uint32_t* __restrict__ kout, uint2* __restrict__ vout) {
   __shared__ uint32_t run_cnt[RADIX];
   __shared__ uint32_t wave_cnt[WAVES][RADIX];
-  __shared__ uint32_t base_off[RADIX];
+  __shared__ uint32_t tile_start[RADIX];
+  __shared__ uint32_t glob_off[RADIX];
+  __shared__ uint16_t perm[SORT_TILE];
   const int t = threadIdx.x, w = t / WAVE, lane = t % WAVE;
+  const int64_t base = (int64_t)blockIdx.x * SORT_TILE;
+  const int cnt = (int)min<int64_t>(SORT_TILE, n - base);
+  // tile histogram, then its exclusive prefix (tile-local start of each digit)
   run_cnt[t] = 0;
-  base_off[t] = offs[(int64_t)t * nblocks + blockIdx.x];
+  __syncthreads();
+  for (int r = 0; r < SORT_ROUNDS; ++r) {
+    const int j = r * THREADS + t;
+    if (j < cnt) atomicAdd(&run_cnt[(kin[base + j] >> shift) & (RADIX - 1)], 1u);
+  }
+  __syncthreads();
+  const uint32_t c = run_cnt[t];
+  wave_cnt[0][t] = c;
+  __syncthreads();
+  for (int off = 1; off < RADIX; off <<= 1) {
+    const uint32_t x = t >= off ? wave_cnt[0][t - off] : 0u;
+    __syncthreads();
+    wave_cnt[0][t] += x;
+    __syncthreads();
+  }
+  tile_start[t] = wave_cnt[0][t] - c;
+  run_cnt[t] = wave_cnt[0][t] - c;
+  glob_off[t] = offs[(int64_t)t * nblocks + blockIdx.x];
+  __syncthreads();
 #pragma unroll
   for (int k = 0; k < WAVES; ++k) wave_cnt[k][t] = 0;
   __syncthreads();
   const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (WAVE - lane));
-  const int64_t base = (int64_t)blockIdx.x * SORT_TILE;
   for (int r = 0; r < SORT_ROUNDS; ++r) {
-    const int64_t i = base + r * THREADS + t;
-    const bool valid = i < n;
-    const uint32_t key = valid ? kin[i] : 0u;
-    const uint2 val = valid ? vin[i] : make_uint2(0, 0);
+    const int j = r * THREADS + t;
+    const bool valid = j < cnt;
+    const uint32_t key = valid ? kin[base + j] : 0u;
     const uint32_t d = (key >> shift) & (RADIX - 1);
     uint64_t match = __ballot(valid);
 #pragma unroll
@@ -1037,100 +1061,104 @@ __global__ void __launch_bounds__(THREADS) k_radix_scatter(const uint32_t* __res
       uint32_t run = run_cnt[t];
 #pragma unroll
       for (int k = 0; k < WAVES; ++k) {
-        const uint32_t c = wave_cnt[k][t];
+        const uint32_t cw = wave_cnt[k][t];
         wave_cnt[k][t] = run;
-        run += c;
+        run += cw;
       }
       run_cnt[t] = run;
     }
     __syncthreads();
-    if (valid) {
-      const uint32_t pos = base_off[d] + wave_cnt[w][d] + (uint32_t)rank;
-      kout[pos] = key;
-      vout[pos] = val;
-    }
+    if (valid) perm[wave_cnt[w][d] + (uint32_t)rank] = (uint16_t)j;
     __syncthreads();
 #pragma unroll
     for (int k = 0; k < WAVES; ++k) wave_cnt[k][t] = 0;
     __syncthreads();
   }
+  // write out in digit order (the tile's inputs are still in cache)
+  for (int r = 0; r < SORT_ROUNDS; ++r) {
+    const int j = r * THREADS + t;
+    if (j < cnt) {
+      const int src = perm[j];
+      const uint32_t key = kin[base + src];
+      const uint32_t d = (key >> shift) & (RADIX - 1);
+      const uint32_t pos = glob_off[d] + (uint32_t)j - tile_start[d];
+      kout[pos] = key;
+      vout[pos] = vin[base + src];
+    }
+  }
 }
 
-// Segmented reduction of the sorted pairs: one wave per 64 consecutive pairs
-// (lane = pair).  Each lane forms w * G[lookup] in column groups of 16, a
-// segmented inclusive scan over the lanes sums every run of equal locations,
-// and the last lane of each run writes the row: a plain read-modify-write when
-// the whole run lies inside these 64 pairs (no other wave touches that row),
-// fp32 atomics for the runs cut by the chunk edges.
+// Segmented reduction of the sorted pairs.  A group of M lanes (lane = column
+// of the gradient row) owns a span of consecutive pairs (256, fewer for small
+// batches so that every CU gets work) and walks it in
+// order, prefetching 16 pairs and their upstream-gradient rows at a time; it
+// accumulates w * G[lookup] while the location stays the same and writes each
+// finished run of one location with a single plain read-modify-write when the
+// run lies inside the span (no other group touches that row), or with fp32
+// atomics for the runs cut by the span edges (so a hot location costs one
+// atomic row per span of updates and never serialises one group).
+constexpr int SEG_SPAN = 256;
+constexpr int SEG_BATCH = 16;
+
+template <int M>
+__device__ __forceinline__ void seg_flush(float* __restrict__ gtab, uint32_t key, int col, float acc, bool plain) {
+  float* dst = gtab + (size_t)key * M + col;
+  if (plain)
+    *dst += acc;
+  else
+    unsafeAtomicAdd(dst, acc);
+}
+
 template <int M>
 __global__ void __launch_bounds__(THREADS) k_segreduce(const uint32_t* __restrict__ keys,
                                                        const uint2* __restrict__ vals, int64_t n, uint32_t N,
-                                                       const float* __restrict__ gout, float* __restrict__ gtab) {
-  const int lane = threadIdx.x % WAVE;
-  const int64_t chunk = (int64_t)blockIdx.x * WAVES + threadIdx.x / WAVE;
-  const int64_t p = chunk * WAVE + lane;
-  if (chunk * WAVE >= n) return;
-  const bool valid = p < n;
-  const uint32_t key = valid ? keys[p] : N;
-  const uint2 val = valid ? vals[p] : make_uint2(0, 0);
-  const uint32_t prev_edge = (lane == 0 && p > 0 && valid) ? keys[p - 1] : 0xFFFFFFFFu;
-  const int64_t pl = chunk * WAVE + WAVE;  // first pair of the next chunk
-  const uint32_t next_edge = (lane == WAVE - 1 && pl < n) ? keys[pl] : 0xFFFFFFFFu;
-  const uint32_t up = __shfl_up(key, 1);
-  const uint32_t down = __shfl_down(key, 1);
-  const bool head = (lane == 0) ? (p == 0 || prev_edge != key) : (up != key);
-  const bool tail = (lane == WAVE - 1) ? (next_edge != key) : (down != key);
-  const bool live = valid && key < N;
-  // head flags of the segmented scan (shared by every column group)
-  bool seen = head;
-  {
-    bool f = head;
+                                                       const float* __restrict__ gout, float* __restrict__ gtab,
+                                                       int span) {
+  const int64_t group = ((int64_t)blockIdx.x * THREADS + threadIdx.x) / M;
+  const int col = threadIdx.x % M;
+  const int64_t b = group * span;
+  if (b >= n) return;
+  const int64_t e = min<int64_t>(n, b + span);
+  uint32_t cur = keys[b];
+  if (cur >= N) return;  // padding sorts last
+  bool head_here = (b == 0) || keys[b - 1] != cur;
+  float acc = 0.0f;
+  bool pad = false;  // reached the padding (key N), which sorts last
+  for (int64_t p = b; p < e && !pad; p += SEG_BATCH) {
+    uint32_t k[SEG_BATCH];
+    float wv[SEG_BATCH], g[SEG_BATCH];
 #pragma unroll
-    for (int off = 1; off < WAVE; off <<= 1) {
-      const bool fo = __shfl_up((int)f, off) != 0;
-      if (lane >= off) f = f || fo;
+    for (int u = 0; u < SEG_BATCH; ++u) {
+      const int64_t q = p + u;
+      k[u] = q < e ? keys[q] : N;
+      const uint2 v = q < e ? vals[q] : make_uint2(0, 0);
+      wv[u] = __uint_as_float(v.y);
+      g[u] = k[u] < N ? gout[(size_t)v.x * M + col] : 0.0f;
     }
-    seen = f;  // a head of this lane's run lies inside the chunk at or before this lane
-  }
-  const bool writer = live && (tail || lane == WAVE - 1);
-  const bool partial = !seen || (lane == WAVE - 1 && !tail);
-  const float wgt = __uint_as_float(val.y);
-  const float* gp = gout + (size_t)val.x * M;
-  float* dst = gtab + (size_t)key * M;
-#pragma unroll 1
-  for (int c0 = 0; c0 < M; c0 += 16) {
-    float v[16];
 #pragma unroll
-    for (int e = 0; e < 16; e += 4) {
-      const float4 g = live ? *reinterpret_cast<const float4*>(gp + c0 + e) : make_float4(0, 0, 0, 0);
-      v[e] = wgt * g.x; v[e + 1] = wgt * g.y; v[e + 2] = wgt * g.z; v[e + 3] = wgt * g.w;
-    }
-    bool f = head;
-#pragma unroll
-    for (int off = 1; off < WAVE; off <<= 1) {
-      const bool fo = __shfl_up((int)f, off) != 0;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float o = __shfl_up(v[e], off);
-        if (lane >= off && !f) v[e] += o;
-      }
-      if (lane >= off) f = f || fo;
-    }
-    if (writer) {
-      if (partial) {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) unsafeAtomicAdd(dst + c0 + e, v[e]);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 16; e += 4) {
-          float4* d4 = reinterpret_cast<float4*>(dst + c0 + e);
-          float4 o = *d4;
-          o.x += v[e]; o.y += v[e + 1]; o.z += v[e + 2]; o.w += v[e + 3];
-          *d4 = o;
+    for (int u = 0; u < SEG_BATCH; ++u) {
+      if (p + u < e && !pad) {
+        if (k[u] >= N) {
+          pad = true;  // the current run ended just before the padding
+        } else {
+          if (k[u] != cur) {
+            seg_flush<M>(gtab, cur, col, acc, head_here);  // ended inside the span
+            cur = k[u];
+            acc = 0.0f;
+            head_here = true;
+          }
+          acc = fmaf(wv[u], g[u], acc);
         }
       }
     }
   }
+  if (pad) {
+    seg_flush<M>(gtab, cur, col, acc, head_here);
+    return;
+  }
+  // the span's last run: plain only if it also ends inside the span
+  const bool ends_here = (e == n) || keys[e] != cur;
+  seg_flush<M>(gtab, cur, col, acc, head_here && ends_here);
 }
 
 // ---------------------------------------------------------------------------
@@ -1279,9 +1307,14 @@ struct BwdSortedLaunch {
       std::swap(kin, kout);
       std::swap(vin, vout);
     }
-    const unsigned chunks = (unsigned)((ws.n + WAVE - 1) / WAVE);
-    hipLaunchKernelGGL((k_segreduce<M>), dim3((chunks + WAVES - 1) / WAVES), dim3(THREADS), 0, s, kin, vin, ws.n,
-                       P.N, g, gt);
+    // span: 256 pairs per group, fewer when that would leave CUs idle (about
+    // 32 groups per CU for 256 CUs)
+    int64_t span = (ws.n + 256 * 32 - 1) / (256 * 32);
+    span = span < SEG_BATCH ? SEG_BATCH : (span > SEG_SPAN ? SEG_SPAN : span);
+    const int64_t groups = (ws.n + span - 1) / span;
+    const int64_t per_block = THREADS / M;
+    hipLaunchKernelGGL((k_segreduce<M>), dim3((unsigned)((groups + per_block - 1) / per_block)), dim3(THREADS), 0, s,
+                       kin, vin, ws.n, P.N, g, gt, (int)span);
     return launched();
   }
 };
