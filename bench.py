@@ -112,7 +112,7 @@ def main():
     ap.add_argument("--steps", type=int, default=15)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="k14-m32-bf16-zipf")
-    ap.add_argument("--mode", default="atomic", choices=["atomic", "sorted"])
+    ap.add_argument("--mode", default="auto", choices=["auto", "atomic", "sorted", "merged"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-compare", action="store_true", help="skip timing the other scatter mode")
@@ -162,10 +162,14 @@ def main():
     log("distinct rows touched: %d of %d slots (%.1f%%)" % (U, w.L * 32, 100.0 * U / (w.L * 32)))
 
     stream = torch.cuda.current_stream()
+    mode = lram.resolved_mode(w.B, w.H, args.mode)
+    log("value-gradient scatter: %s" % mode)
+    nbytes = lram.backward_workspace_bytes(w.B, w.H, w.m, mode)
+    wsp = torch.empty(nbytes, dtype=torch.uint8, device=dev) if nbytes else None
 
     def step():
         lram.forward(q, table, w.K, out=out)
-        lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, mode=args.mode)
+        lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, mode=mode, workspace=wsp)
 
     for i in range(args.warmup):
         step()
@@ -178,7 +182,7 @@ def main():
         ev[k][0].record(stream)
         lram.forward(q, table, w.K, out=out)
         ev[k][1].record(stream)
-        lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, mode=args.mode)
+        lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, mode=mode, workspace=wsp)
         ev[k][2].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
@@ -187,13 +191,14 @@ def main():
     ms_step = wall * 1e3 / args.steps
     log("timed %d steps: %.3f ms/step (forward %.3f ms, backward %.3f ms)" % (args.steps, ms_step, fwd_ms, bwd_ms))
 
-    # the other value-gradient scatter, timed the same way for comparison (not part of `value`)
-    other = "sorted" if args.mode == "atomic" else "atomic"
-    other_ms = None
-    if not args.no_compare:
-        ws = None
-        if other == "sorted":
-            ws = torch.empty(lram.backward_workspace_bytes(w.B, w.H, w.m, "sorted"), dtype=torch.uint8, device=dev)
+    # the other value-gradient scatters, timed the same way for comparison (not part of `value`)
+    by_scatter = {mode: bwd_ms}
+    del wsp
+    for other in ("atomic", "sorted", "merged"):
+        if other == mode or args.no_compare:
+            continue
+        nbytes = lram.backward_workspace_bytes(w.B, w.H, w.m, other)
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=dev) if nbytes else None
         lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, mode=other, workspace=ws)
         torch.cuda.synchronize()
         e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
@@ -202,9 +207,9 @@ def main():
             lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, mode=other, workspace=ws)
         e[1].record(stream)
         torch.cuda.synchronize()
-        other_ms = e[0].elapsed_time(e[1]) / 5
+        by_scatter[other] = e[0].elapsed_time(e[1]) / 5
         del ws
-        log("backward with the %s scatter: %.3f ms" % (other, other_ms))
+        log("backward with the %s scatter: %.3f ms" % (other, by_scatter[other]))
 
     st = 4 if w.dtype == "f32" else 2
     L = w.L
@@ -213,7 +218,11 @@ def main():
     fwd_req = L * (32 + w.m * st + 32 * w.m * st)
     bwd_req = L * (32 + w.m * 4 + 32 + 32 * (w.m * st + 2 * w.m * 4))
     if bwd_ms >= fwd_ms:
-        kname, kms, kbytes, kreq = "k_backward_atomic", bwd_ms, bwd_bytes, bwd_req
+        # the atomic backward is one kernel; the other modes time their whole
+        # pass (lookup/location sort + fused kernel) between the same events
+        kname = {"atomic": "k_backward_atomic", "merged": "backward_pass_merged",
+                 "sorted": "backward_pass_sorted"}[mode]
+        kms, kbytes, kreq = bwd_ms, bwd_bytes, bwd_req
     else:
         kname, kms, kbytes, kreq = "k_forward", fwd_ms, fwd_bytes, fwd_req
     achieved = kbytes / (kms * 1e-3) / 1e9
@@ -232,11 +241,11 @@ def main():
         "dtype": "bf16 table, fp32 accumulate" if w.dtype == "bf16" else "f32",
         "data": "synthetic (seeded; see workloads.py)",
         "config": {"workload": w.name, "K": list(w.K), "locations": w.N, "m": w.m, "table_dtype": w.dtype,
-                   "batch": w.B, "heads": w.H, "lookups": L, "scatter": args.mode, "parallelism": "none (1 GPU)"},
+                   "batch": w.B, "heads": w.H, "lookups": L, "scatter": mode, "parallelism": "none (1 GPU)"},
         "fwd_lookups_per_s": L / (fwd_ms * 1e-3),
         "fwd_ms": fwd_ms,
         "bwd_ms": bwd_ms,
-        "bwd_ms_by_scatter": {args.mode: bwd_ms, other: other_ms},
+        "bwd_ms_by_scatter": by_scatter,
         "distinct_rows": U,
         "roofline": {"kernel": kname, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,

@@ -16,7 +16,9 @@
  *     q_i in [0, K_i) covers it once; the lattice work happens at the doubled
  *     scale of Sec. 2.4, x_i = fmodf(2 q_i, 2 K_i) (exact; a negative q_i keeps
  *     its sign; any real q_i is accepted).
- *   - K.  Eight even integers K_i >= 2 (host array); N = prod K_i < 2^31.
+ *   - K.  Eight even integers 2 <= K_i <= 8192 (host array); N = prod K_i < 2^31.
+ *     (8192 keeps every lattice coordinate of the doubled scale inside int16;
+ *     with N < 2^31 it only excludes tori that are nearly one-dimensional.)
  *   - Locations.  slot(k) = eps*N/2 + ((..(Y_0 K_1 + Y_1) K_2 + ..) K_6 + Y_6)*(K_7/2)
  *     + floor(Y_7/2), with eps = k_0 mod 2 and Y_i = ((k_i - eps)/2) mod K_i:
  *     row slot of the value table holds v at that location (Sec. 2.2, M = Lambda/L_K).
@@ -57,7 +59,7 @@ extern "C" {
 typedef enum {
   LRAM_OK = 0,
   LRAM_EINVAL = 1,      /* null pointer with L > 0, negative size, misaligned pointer */
-  LRAM_EBADK = 2,       /* a K_i odd or < 2, N != prod K, or N >= 2^31 */
+  LRAM_EBADK = 2,       /* a K_i odd, < 2 or > 8192, N != prod K, or N >= 2^31 */
   LRAM_EDTYPE = 3,      /* unknown dtype or unsupported m for that dtype */
   LRAM_EWORKSPACE = 4,  /* workspace missing or smaller than lram_backward_workspace_bytes */
   LRAM_EMODE = 5,       /* unknown scatter mode */
@@ -68,7 +70,10 @@ typedef enum { LRAM_F32 = 0, LRAM_BF16 = 1 } lram_dtype;
 
 typedef enum {
   LRAM_SCATTER_ATOMIC = 0, /* fp32 atomic adds straight into grad_table */
-  LRAM_SCATTER_SORTED = 1  /* sort (slot, lookup) pairs, one read-modify-write per touched row */
+  LRAM_SCATTER_SORTED = 1, /* sort (slot, lookup) pairs, one read-modify-write per touched row */
+  LRAM_SCATTER_MERGED = 2, /* order lookups by their closest lattice point, merge equal slots within
+                              each batch of 64 consecutive lookups, one atomic row per distinct slot */
+  LRAM_SCATTER_AUTO = 3    /* MERGED for L >= 131072 lookups, ATOMIC below (the sort does not pay off) */
 } lram_scatter_mode;
 
 /* Library version (major*10000 + minor*100 + patch). */
@@ -107,6 +112,12 @@ int lram_forward(const float* q, int64_t B, int64_t H, const int32_t K[8], const
 int lram_backward_workspace_bytes(int64_t B, int64_t H, int32_t m, int mode, size_t* bytes);
 
 /*
+ * lram_scatter_mode_resolved -- the concrete mode (ATOMIC, SORTED or MERGED)
+ * that lram_backward runs for L = B*H lookups when given `mode` (host only).
+ */
+int lram_scatter_mode_resolved(int64_t B, int64_t H, int mode, int* resolved);
+
+/*
  * lram_backward -- gradients of sum_l <grad_out[l], phi(q_l)> with the selection
  * held fixed (Sec. 2.6: the kernel supplies the weights and their derivatives
  * to an autograd wrapper):
@@ -120,7 +131,8 @@ int lram_backward_workspace_bytes(int64_t B, int64_t H, int32_t m, int mode, siz
  * The neighbour search is recomputed from q.  workspace/ws_bytes: device
  * buffer, 256-byte aligned, of at least lram_backward_workspace_bytes (may be
  * NULL for the atomic mode); its contents on entry do not matter.  The sorted
- * mode needs 32 L < 2^32.  grad_table may be NULL only if grad_q is not.
+ * and merged modes need 32 L < 2^32.  grad_table may be NULL only if grad_q is
+ * not (without grad_table every mode computes grad_q the same way).
  */
 int lram_backward(const float* q, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
                   int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_q, int mode,

@@ -20,13 +20,14 @@ from typing import Optional, Sequence, Tuple
 import torch  # noqa: F401  -- loads the HIP runtime liblram.so must share
 
 __all__ = ["neighbors", "forward", "backward", "backward_workspace_bytes", "lookup", "LramLookup",
-           "library_path", "load", "LramError", "F32", "BF16", "SCATTER_ATOMIC", "SCATTER_SORTED", "NB"]
+           "library_path", "load", "LramError", "F32", "BF16", "SCATTER_ATOMIC", "SCATTER_SORTED",
+           "SCATTER_MERGED", "SCATTER_AUTO", "resolved_mode", "NB"]
 
 NB = 32
 F32, BF16 = 0, 1
-SCATTER_ATOMIC, SCATTER_SORTED = 0, 1
-_MODES = {"atomic": SCATTER_ATOMIC, "sorted": SCATTER_SORTED, SCATTER_ATOMIC: SCATTER_ATOMIC,
-          SCATTER_SORTED: SCATTER_SORTED}
+SCATTER_ATOMIC, SCATTER_SORTED, SCATTER_MERGED, SCATTER_AUTO = 0, 1, 2, 3
+_MODE_NAMES = {"atomic": SCATTER_ATOMIC, "sorted": SCATTER_SORTED, "merged": SCATTER_MERGED, "auto": SCATTER_AUTO}
+_MODES = {**_MODE_NAMES, **{v: v for v in _MODE_NAMES.values()}}
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "_build", "liblram.so")
@@ -61,6 +62,8 @@ def load():
             lib.lram_forward.restype = I
             lib.lram_backward_workspace_bytes.argtypes = [I64, I64, I32, I, ctypes.POINTER(ctypes.c_size_t)]
             lib.lram_backward_workspace_bytes.restype = I
+            lib.lram_scatter_mode_resolved.argtypes = [I64, I64, I, ctypes.POINTER(ctypes.c_int)]
+            lib.lram_scatter_mode_resolved.restype = I
             lib.lram_backward.argtypes = [P, I64, I64, P, P, I, I64, I32, P, P, P, I, P, ctypes.c_size_t, P]
             lib.lram_backward.restype = I
             _lib = lib
@@ -138,7 +141,15 @@ def forward(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], out: Optiona
     return out
 
 
-def backward_workspace_bytes(B: int, H: int, m: int, mode="atomic") -> int:
+def resolved_mode(B: int, H: int, mode="auto") -> str:
+    """Name of the scatter mode lram_backward runs for B*H lookups given ``mode``."""
+    lib = load()
+    r = ctypes.c_int(-1)
+    _check(lib.lram_scatter_mode_resolved(B, H, _MODES[mode], ctypes.byref(r)))
+    return {v: k for k, v in _MODE_NAMES.items()}[r.value]
+
+
+def backward_workspace_bytes(B: int, H: int, m: int, mode="auto") -> int:
     lib = load()
     n = ctypes.c_size_t(0)
     _check(lib.lram_backward_workspace_bytes(B, H, m, _MODES[mode], ctypes.byref(n)))
@@ -146,7 +157,7 @@ def backward_workspace_bytes(B: int, H: int, m: int, mode="atomic") -> int:
 
 
 def backward(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], grad_out: torch.Tensor,
-             grad_table: Optional[torch.Tensor] = None, want_grad_q: bool = True, mode="atomic",
+             grad_table: Optional[torch.Tensor] = None, want_grad_q: bool = True, mode="auto",
              workspace: Optional[torch.Tensor] = None, grad_q: Optional[torch.Tensor] = None):
     """Gradients: grad_table [N, m] fp32 is ACCUMULATED into (allocated zeroed if None,
     pass False to skip), grad_q [..., 8] fp32 (None unless want_grad_q; written into
@@ -191,5 +202,5 @@ class LramLookup(torch.autograd.Function):
         return gq, (gt.to(table.dtype) if gt is not None else None), None, None
 
 
-def lookup(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], mode="atomic") -> torch.Tensor:
+def lookup(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], mode="auto") -> torch.Tensor:
     return LramLookup.apply(q, table, tuple(K), mode)

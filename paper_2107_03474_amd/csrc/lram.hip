@@ -80,19 +80,25 @@ struct alignas(16) Nbr {
 };
 
 struct alignas(16) WaveLds {
-  Frame frames[WAVE];
   Nbr nbr[2][NB];     // double-buffered: lookup t+1 is searched while t is consumed
   float wgt[2][NB];
   uint32_t tie[TIE_MAX][2];
   uint32_t hist[64];  // distance histogram of the selection, 64 buckets on [4, 8)
 };
 
-struct alignas(16) BlockLds {
-  // per-query tables, [coordinate i][wave w][value v] -> byte i*256 + w*64 + 4v
+// per-query tables, [coordinate i][wave w][value v] -> byte i*256 + w*64 + 4v
+struct alignas(16) Tables {
   float qt[8 * 64];
   uint32_t st[8 * 64];
   float et[8 * 64];
+};
+
+// LDS of the search for FR lookups per wave.
+template <int FR>
+struct alignas(16) SearchLds {
+  Tables tab;
   WaveLds wave[WAVES];
+  Frame frames[WAVES][FR];
 };
 
 __device__ __forceinline__ float lds_f32(const float* base, uint32_t byte_off) {
@@ -154,8 +160,10 @@ __device__ __forceinline__ void d8_round(const float (&y)[8], int (&r)[8]) {
   }
 }
 
-__device__ __forceinline__ void make_frame(const float* __restrict__ q, bool have, const Params P, Frame& F) {
-  float x[8];
+// Wrapped Lambda-scale query x and the closest point c of Lambda (either coset);
+// false for a non-finite query (x = 0 then).
+__device__ __forceinline__ bool closest_point(const float* __restrict__ q, bool have, const Params P, float (&x)[8],
+                                              int (&c)[8]) {
   bool valid = have;
   if (have) {
     float4 a = reinterpret_cast<const float4*>(q)[0];
@@ -192,12 +200,19 @@ __device__ __forceinline__ void make_frame(const float* __restrict__ q, bool hav
     d1 += e1 * e1;
   }
   const bool odd = d1 < d0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) c[i] = odd ? 2 * r1[i] + 1 : 2 * r0[i];
+  return valid;
+}
+
+__device__ __forceinline__ void make_frame(const float* __restrict__ q, bool have, const Params P, Frame& F) {
+  float x[8];
   int c[8];
+  const bool valid = closest_point(q, have, P, x, c);
   float a[8];
   uint32_t neg = 0;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    c[i] = odd ? 2 * r1[i] + 1 : 2 * r0[i];
     float y = x[i] - (float)c[i];
     a[i] = fabsf(y);
     neg |= (y < 0.0f ? 1u : 0u) << i;
@@ -431,7 +446,7 @@ __device__ __forceinline__ int threshold32_hist(const uint32_t (&key)[NS], uint3
 }
 
 struct Search {
-  BlockLds& S;
+  Tables& S;
   WaveLds& W;
   int lane;
   uint32_t wbyte;
@@ -443,8 +458,8 @@ struct Search {
 
   // (the kernel argument is read field by field: holding a reference to it
   // would force the argument block into private memory)
-  __device__ Search(const Params P, BlockLds& s, int w, int l)
-      : S(s), W(s.wave[w]), lane(l), wbyte(64u * (uint32_t)w) {
+  __device__ Search(const Params P, Tables& s, WaveLds& wv, int w, int l)
+      : S(s), W(wv), lane(l), wbyte(64u * (uint32_t)w) {
 #pragma unroll
     for (int k = 0; k < NS_STRICT; ++k) load_candidate<0>(lane + WAVE * k, wbyte, lo[k], hi[k]);
     ti = lane >> 3;
@@ -608,9 +623,22 @@ struct Search {
 
 // Phase A for the wave's lookups [base, base + lpw).
 __device__ __forceinline__ void phase_a(const float* __restrict__ q, int64_t base, int nl, const Params P,
-                                        WaveLds& W, int lane) {
-  if (lane < nl) make_frame(q + (base + lane) * 8, true, P, W.frames[lane]);
+                                        Frame* frames, int lane) {
+  if (lane < nl) make_frame(q + (base + lane) * 8, true, P, frames[lane]);
   wave_lds_sync();
+}
+
+// Same, for the lookups perm[base .. base + nl) of a reordered batch; returns
+// this lane's lookup index (lane t holds the lookup of position base + t).
+__device__ __forceinline__ uint32_t phase_a_perm(const float* __restrict__ q, const uint2* __restrict__ perm,
+                                                 int64_t base, int nl, const Params P, Frame* frames, int lane) {
+  uint32_t l = 0;
+  if (lane < nl) {
+    l = perm[base + lane].x;
+    make_frame(q + (size_t)l * 8, true, P, frames[lane]);
+  }
+  wave_lds_sync();
+  return l;
 }
 
 // ---------------------------------------------------------------------------
@@ -634,14 +662,15 @@ __device__ __forceinline__ bool wave_ctx(const Params P, WaveCtx& c) {
 __global__ void __launch_bounds__(THREADS) k_neighbors(const float* __restrict__ q, Params P,
                                                        int32_t* __restrict__ slot_out, float* __restrict__ w_out,
                                                        float* __restrict__ d2_out) {
-  __shared__ BlockLds S;
+  __shared__ SearchLds<WAVE> S;
   WaveCtx c;
   if (!wave_ctx(P, c)) return;
-  Search srch(P, S, c.wave, c.lane);
+  Search srch(P, S.tab, S.wave[c.wave], c.wave, c.lane);
   WaveLds& W = S.wave[c.wave];
-  phase_a(q, c.base, c.nl, P, W, c.lane);
+  Frame* FR = S.frames[c.wave];
+  phase_a(q, c.base, c.nl, P, FR, c.lane);
   for (int t = 0; t < c.nl; ++t) {
-    const Frame& F = W.frames[t];
+    const Frame& F = FR[t];
     const Sel sel = read_sel(F);
     const int count = srch.run(F, sel, 0);
     const int64_t l = c.base + t;
@@ -773,135 +802,148 @@ template <int DT, int M>
 __global__ void __launch_bounds__(THREADS) k_forward(const float* __restrict__ q, Params P,
                                                      const void* __restrict__ table, void* __restrict__ out) {
   using G = FwdGeom<DT, M>;
-  __shared__ BlockLds S;
+  __shared__ SearchLds<WAVE> S;
   WaveCtx c;
   if (!wave_ctx(P, c)) return;
-  Search srch(P, S, c.wave, c.lane);
+  Search srch(P, S.tab, S.wave[c.wave], c.wave, c.lane);
   WaveLds& W = S.wave[c.wave];
-  phase_a(q, c.base, c.nl, P, W, c.lane);
+  Frame* FR = S.frames[c.wave];
+  phase_a(q, c.base, c.nl, P, FR, c.lane);
   const char* tb = reinterpret_cast<const char*>(table);
   uint32_t v[G::NI][G::DW];
-  srch.run(W.frames[0], read_sel(W.frames[0]), 0);
+  srch.run(FR[0], read_sel(FR[0]), 0);
   fwd_issue<DT, M>(tb, W, 0, c.lane, v);
   for (int t = 0; t < c.nl; ++t) {
     const int buf = t & 1;
     // search lookup t+1 while the rows of lookup t are in flight
-    if (t + 1 < c.nl) srch.run(W.frames[t + 1], read_sel(W.frames[t + 1]), buf ^ 1);
+    if (t + 1 < c.nl) srch.run(FR[t + 1], read_sel(FR[t + 1]), buf ^ 1);
     fwd_consume<DT, M>(W, buf, c.lane, c.base + t, v, out);
     if (t + 1 < c.nl) fwd_issue<DT, M>(tb, W, buf ^ 1, c.lane, v);
   }
 }
 
 // Backward, fused with the query gradient: per lookup, read the 32 rows once
-// for <G, v_j> and form dq from the coordinate errors.  The value gradient is
-// either added straight into grad_table with fp32 atomics (EMIT = false), or
-// emitted as (location, (lookup, w_j)) pairs for the sorted segmented
-// reduction (EMIT = true; padding gets the key N, which sorts last).
+// for <G, v_j> and form dq from the coordinate errors.
+
+// Value-gradient scatter of one lookup: M consecutive lanes own one gradient
+// row, so each atomic instruction covers 64/M whole rows.
+template <int M>
+__device__ __forceinline__ void scatter_atomic(const WaveLds& W, const float* __restrict__ gout, int64_t l,
+                                               float* __restrict__ gtab, int lane) {
+  constexpr int RA = WAVE / M;
+  const int col = lane % M;
+  const float gc = gout[(size_t)l * M + col];
+#pragma unroll 4
+  for (int k = 0; k < NB / RA; ++k) {
+    const int j = k * RA + lane / M;
+    const int32_t s = W.nbr[0][j].slot;
+    if (s >= 0) unsafeAtomicAdd(gtab + (size_t)s * M + col, W.wgt[0][j] * gc);
+  }
+}
+
+// dq_i = sum_j -2 u_j^3 (x_i - k_{j,i}) <G, v_j> of one lookup (zero without
+// neighbours), written to gq[l].
+template <int DT, int M>
+__device__ __forceinline__ void grad_query(const Frame& F, const WaveLds& W, const Tables& T, int count,
+                                           const char* __restrict__ tb, const float* __restrict__ gout, int64_t l,
+                                           int lane, float* __restrict__ gq) {
+  using G = RowGeom<DT, M>;
+  constexpr int ICOORD = G::LPR >= 8 ? 1 : 8 / G::LPR;  // query coordinates per lane
+  const int rsub = lane / G::LPR, ch = lane % G::LPR;
+  float dq[ICOORD];
+#pragma unroll
+  for (int k = 0; k < ICOORD; ++k) dq[k] = 0.0f;
+  if (count > 0) {
+    float g[G::EPC];
+    const float* gp = gout + (size_t)l * M + ch * G::EPC;
+#pragma unroll
+    for (int e = 0; e < G::EPC; e += 4) {
+      const float4 gv = *reinterpret_cast<const float4*>(gp + e);
+      g[e] = gv.x; g[e + 1] = gv.y; g[e + 2] = gv.z; g[e + 3] = gv.w;
+    }
+    // per-lane selectors of the query coordinates this lane accumulates
+    uint32_t lsel[ICOORD];
+#pragma unroll
+    for (int k = 0; k < ICOORD; ++k) {
+      lsel[k] = F.sel[(ch + k * G::LPR) & 7];
+    }
+    uint4 v[G::NP];
+    int32_t sl[G::NP];
+#pragma unroll
+    for (int p = 0; p < G::NP; ++p) {
+      sl[p] = W.nbr[0][p * G::RPP + rsub].slot;
+      v[p] = sl[p] >= 0 ? *reinterpret_cast<const uint4*>(tb + (size_t)sl[p] * G::RB + ch * 16)
+                        : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int p = 0; p < G::NP; ++p) {
+      const int j = p * G::RPP + rsub;
+      float f[G::EPC];
+      unpack16<DT, G::EPC>(v[p], f);
+      float pd = 0.0f;
+#pragma unroll
+      for (int e = 0; e < G::EPC; ++e) pd = fmaf(g[e], f[e], pd);
+      // <G, v_j>: sum over the LPR lanes of this row
+#pragma unroll
+      for (int mask = 1; mask < G::LPR; mask <<= 1) pd += __shfl_xor(pd, mask);
+      if (sl[p] >= 0) {
+        const Nbr n = W.nbr[0][j];
+        const float u = 1.0f - __uint_as_float(n.dbits) * 0.125f;
+        const float a = -2.0f * u * u * u * pd;
+#pragma unroll
+        for (int k = 0; k < ICOORD; ++k) {
+          const int i = ch + k * G::LPR;
+          if (i < 8) {
+            const uint32_t ab = __builtin_amdgcn_perm(n.hi, n.lo, lsel[k]);
+            dq[k] = fmaf(a, lds_f32(T.et, ab + 256u * i), dq[k]);
+          }
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int mask = G::LPR; mask < WAVE; mask <<= 1)
+#pragma unroll
+    for (int k = 0; k < ICOORD; ++k) dq[k] += __shfl_xor(dq[k], mask);
+  if (rsub == 0) {
+#pragma unroll
+    for (int k = 0; k < ICOORD; ++k) {
+      const int i = ch + k * G::LPR;
+      if (i < 8) gq[l * 8 + i] = dq[k];
+    }
+  }
+}
+
+// The value gradient is either added straight into grad_table with fp32
+// atomics (EMIT = false), or emitted as (location, (lookup, w_j)) pairs for
+// the sorted segmented reduction (EMIT = true; padding gets the key N, which
+// sorts last).
 template <int DT, int M, bool EMIT>
 __global__ void __launch_bounds__(THREADS) k_backward(const float* __restrict__ q, Params P,
                                                       const void* __restrict__ table,
                                                       const float* __restrict__ gout, float* __restrict__ gtab,
                                                       float* __restrict__ gq, uint32_t* __restrict__ pair_key,
                                                       uint2* __restrict__ pair_val) {
-  using G = RowGeom<DT, M>;
-  constexpr int ICOORD = G::LPR >= 8 ? 1 : 8 / G::LPR;  // query coordinates per lane
-  __shared__ BlockLds S;
+  __shared__ SearchLds<WAVE> S;
   WaveCtx c;
   if (!wave_ctx(P, c)) return;
   const int lane = c.lane;
-  Search srch(P, S, c.wave, lane);
+  Search srch(P, S.tab, S.wave[c.wave], c.wave, lane);
   WaveLds& W = S.wave[c.wave];
-  phase_a(q, c.base, c.nl, P, W, lane);
-  const int rsub = lane / G::LPR, ch = lane % G::LPR;
+  Frame* FR = S.frames[c.wave];
+  phase_a(q, c.base, c.nl, P, FR, lane);
   const char* tb = reinterpret_cast<const char*>(table);
   for (int t = 0; t < c.nl; ++t) {
-    const Frame& F = W.frames[t];
+    const Frame& F = FR[t];
     const Sel sel = read_sel(F);
     const int count = srch.run(F, sel, 0);
     const int64_t l = c.base + t;
-    float dq[ICOORD];
-#pragma unroll
-    for (int k = 0; k < ICOORD; ++k) dq[k] = 0.0f;
-    if (count > 0) {
-      // value-gradient scatter: M consecutive lanes own one gradient row, so each
-      // atomic instruction covers 64/M whole rows
-      if (!EMIT && gtab) {
-        constexpr int RA = WAVE / M;
-        const int col = lane % M;
-        const float gc = gout[(size_t)l * M + col];
-#pragma unroll 4
-        for (int k = 0; k < NB / RA; ++k) {
-          const int j = k * RA + lane / M;
-          const int32_t s = W.nbr[0][j].slot;
-          if (s >= 0) unsafeAtomicAdd(gtab + (size_t)s * M + col, W.wgt[0][j] * gc);
-        }
-      }
-      if (gq) {
-        float g[G::EPC];
-        const float* gp = gout + (size_t)l * M + ch * G::EPC;
-#pragma unroll
-        for (int e = 0; e < G::EPC; e += 4) {
-          const float4 gv = *reinterpret_cast<const float4*>(gp + e);
-          g[e] = gv.x; g[e + 1] = gv.y; g[e + 2] = gv.z; g[e + 3] = gv.w;
-        }
-        // per-lane selectors of the query coordinates this lane accumulates
-        uint32_t lsel[ICOORD];
-#pragma unroll
-        for (int k = 0; k < ICOORD; ++k) {
-          lsel[k] = F.sel[(ch + k * G::LPR) & 7];
-        }
-        uint4 v[G::NP];
-        int32_t sl[G::NP];
-#pragma unroll
-        for (int p = 0; p < G::NP; ++p) {
-          sl[p] = W.nbr[0][p * G::RPP + rsub].slot;
-          v[p] = sl[p] >= 0 ? *reinterpret_cast<const uint4*>(tb + (size_t)sl[p] * G::RB + ch * 16)
-                            : make_uint4(0, 0, 0, 0);
-        }
-#pragma unroll
-        for (int p = 0; p < G::NP; ++p) {
-          const int j = p * G::RPP + rsub;
-          float f[G::EPC];
-          unpack16<DT, G::EPC>(v[p], f);
-          float pd = 0.0f;
-#pragma unroll
-          for (int e = 0; e < G::EPC; ++e) pd = fmaf(g[e], f[e], pd);
-          // <G, v_j>: sum over the LPR lanes of this row
-#pragma unroll
-          for (int mask = 1; mask < G::LPR; mask <<= 1) pd += __shfl_xor(pd, mask);
-          if (sl[p] >= 0) {
-            const Nbr n = W.nbr[0][j];
-            const float u = 1.0f - __uint_as_float(n.dbits) * 0.125f;
-            const float a = -2.0f * u * u * u * pd;
-#pragma unroll
-            for (int k = 0; k < ICOORD; ++k) {
-              const int i = ch + k * G::LPR;
-              if (i < 8) {
-                const uint32_t ab = __builtin_amdgcn_perm(n.hi, n.lo, lsel[k]);
-                dq[k] = fmaf(a, lds_f32(S.et, ab + 256u * i), dq[k]);
-              }
-            }
-          }
-        }
-      }
-    }
+    if (!EMIT && gtab && count > 0) scatter_atomic<M>(W, gout, l, gtab, lane);
+    if (gq) grad_query<DT, M>(F, W, S.tab, count, tb, gout, l, lane, gq);
     if (EMIT && gtab && lane < NB) {
       const int32_t s = W.nbr[0][lane].slot;
       pair_key[l * NB + lane] = s >= 0 ? (uint32_t)s : P.N;
       pair_val[l * NB + lane] = make_uint2((uint32_t)l, __float_as_uint(W.wgt[0][lane]));
-    }
-    if (gq) {
-#pragma unroll
-      for (int mask = G::LPR; mask < WAVE; mask <<= 1)
-#pragma unroll
-        for (int k = 0; k < ICOORD; ++k) dq[k] += __shfl_xor(dq[k], mask);
-      if (rsub == 0) {
-#pragma unroll
-        for (int k = 0; k < ICOORD; ++k) {
-          const int i = ch + k * G::LPR;
-          if (i < 8) gq[l * 8 + i] = dq[k];
-        }
-      }
     }
     wave_lds_sync();
   }
@@ -1162,6 +1204,243 @@ __global__ void __launch_bounds__(THREADS) k_segreduce(const uint32_t* __restric
 }
 
 // ---------------------------------------------------------------------------
+// Batch-merged scatter.  Lookups whose queries share the closest lattice point
+// share most of their 32 neighbours; the lookups are ordered by that point's
+// location (radix sort above), the backward emits (location, w) pairs in that
+// order, and each batch of MERGE_T consecutive lookups is reduced in LDS to one
+// fp32 atomic row per distinct location of the batch.
+
+// key[l] = location of the closest point of Lambda to q_l (N for a non-finite
+// query), val[l] = (l, 0).
+__global__ void __launch_bounds__(THREADS) k_cell_key(const float* __restrict__ q, Params P,
+                                                      uint32_t* __restrict__ key, uint2* __restrict__ val) {
+  const int64_t l = (int64_t)blockIdx.x * THREADS + threadIdx.x;
+  if (l >= P.L) return;
+  float x[8];
+  int c[8];
+  const bool valid = closest_point(q + l * 8, true, P, x, c);
+  uint32_t loc = P.N;
+  if (valid) {
+    const int eps = c[0] & 1;
+    uint32_t acc = eps ? P.N : 0u;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      int y = (c[i] - eps) >> 1;  // in [-1, K_i]
+      y = y < 0 ? y + P.K[i] : (y >= P.K[i] ? y - P.K[i] : y);
+      acc += (uint32_t)y * P.S[i];
+    }
+    loc = acc >> 1;
+  }
+  key[l] = loc;
+  val[l] = make_uint2((uint32_t)l, 0u);
+}
+
+constexpr int64_t AUTO_MERGE_MIN = 131072;      // LRAM_SCATTER_AUTO merges from this many lookups on
+constexpr int MERGE_T = 64;                     // lookups per batch (one workgroup)
+constexpr int MERGE_LPW = MERGE_T / WAVES;      // lookups per wave
+constexpr int MERGE_P = MERGE_T * NB;           // pairs per batch
+constexpr int MERGE_H = 2 * MERGE_P;            // hash entries (load factor <= 1/2)
+constexpr int MERGE_HBITS = 12;
+static_assert((1 << MERGE_HBITS) == MERGE_H, "hash size");
+constexpr int MERGE_PPT = MERGE_P / THREADS;    // pairs per thread
+constexpr int MERGE_HPT = MERGE_H / THREADS;    // hash entries per thread (consecutive)
+constexpr int32_t MERGE_EMPTY = -1;
+static_assert(MERGE_T <= 256 && MERGE_P < 65536, "batch-local indices are 8 and 16 bits wide");
+
+template <int M>
+struct alignas(16) MergeWork {
+  int32_t tag[MERGE_H];         // location of each hash entry; later pair weights and lookups in group order
+  uint32_t cnt[MERGE_H / 2];    // 16-bit pair count of each entry, then its first position in group order
+  float g[MERGE_T][M];          // upstream gradient rows of the batch
+  uint32_t wsum[WAVES][2];
+  uint32_t ngroups;
+};
+
+template <int M>
+struct alignas(16) FusedLds {
+  union {
+    struct {
+      int32_t loc[MERGE_P];     // (location, w) of every pair, [lookup in batch][j]
+      float w[MERGE_P];
+    } pairs;
+    struct {
+      int32_t loc[MERGE_P];     // distinct locations of the batch
+      uint16_t start[MERGE_P + 2];  // first position of each location's pairs in group order
+    } grp;
+  } a;
+  union {
+    SearchLds<MERGE_LPW> search;
+    MergeWork<M> merge;
+  } b;
+};
+
+// One workgroup = one batch of MERGE_T consecutive positions of the order
+// perm: each wave searches MERGE_LPW lookups (with dq as in k_backward) and
+// leaves their (location, w) pairs in LDS; then the workgroup hashes the
+// pairs by location, lays them out grouped by location, and M lanes per
+// distinct location sum w * G over its pairs and add the row with fp32 atomics.
+// Several workgroups per CU overlap one's search with another's atomics.
+// A batch in which fewer than a tenth of the lookups share their closest
+// point with a neighbour in the order (queries spread thinly over the torus)
+// has little to merge: it scatters with per-lookup atomics instead.
+template <int DT, int M>
+__global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __restrict__ q, Params P,
+                                                             const void* __restrict__ table,
+                                                             const float* __restrict__ gout,
+                                                             float* __restrict__ gtab, float* __restrict__ gq,
+                                                             const uint32_t* __restrict__ skey,
+                                                             const uint2* __restrict__ perm) {
+  __shared__ FusedLds<M> S;
+  const int t = threadIdx.x, wave = t / WAVE, lane = t % WAVE;
+  const int64_t bbase = (int64_t)blockIdx.x * (WAVES * P.lpw);
+  const int nt = (int)min<int64_t>(WAVES * P.lpw, P.L - bbase);
+  bool shared = false;
+  if (t < nt) {
+    const uint32_t k = skey[bbase + t];
+    shared = (t > 0 && skey[bbase + t - 1] == k) || (t + 1 < nt && skey[bbase + t + 1] == k);
+  }
+  const bool merge = 10 * __syncthreads_count(shared) >= nt;
+  {
+    const int64_t base = bbase + (int64_t)wave * P.lpw;
+    const int nl = (int)max<int64_t>(0, min<int64_t>(P.lpw, P.L - base));
+    if (nl > 0) {
+      Search srch(P, S.b.search.tab, S.b.search.wave[wave], wave, lane);
+      WaveLds& W = S.b.search.wave[wave];
+      Frame* FR = S.b.search.frames[wave];
+      const uint32_t my_l = phase_a_perm(q, perm, base, nl, P, FR, lane);
+      const char* tb = reinterpret_cast<const char*>(table);
+      for (int i = 0; i < nl; ++i) {
+        const Frame& F = FR[i];
+        const Sel sel = read_sel(F);
+        const int count = srch.run(F, sel, 0);
+        const int64_t l = (int64_t)__builtin_amdgcn_readlane(my_l, i);
+        if (!merge && count > 0) scatter_atomic<M>(W, gout, l, gtab, lane);
+        if (gq) grad_query<DT, M>(F, W, S.b.search.tab, count, tb, gout, l, lane, gq);
+        if (merge && lane < NB) {
+          const int pidx = (wave * P.lpw + i) * NB + lane;
+          S.a.pairs.loc[pidx] = W.nbr[0][lane].slot;
+          S.a.pairs.w[pidx] = W.wgt[0][lane];
+        }
+        wave_lds_sync();
+      }
+    }
+  }
+  if (!merge) return;  // uniform across the workgroup
+  __syncthreads();
+  MergeWork<M>& MW = S.b.merge;
+#pragma unroll
+  for (int k = 0; k < MERGE_HPT; ++k) MW.tag[k * THREADS + t] = MERGE_EMPTY;
+#pragma unroll
+  for (int k = 0; k < MERGE_HPT / 2; ++k) MW.cnt[k * THREADS + t] = 0u;
+  for (int i = t; i < nt * (M / 4); i += THREADS) {
+    const int r = i / (M / 4), c4 = i % (M / 4);
+    const uint32_t l = perm[bbase + r].x;
+    reinterpret_cast<float4*>(MW.g[r])[c4] = reinterpret_cast<const float4*>(gout + (size_t)l * M)[c4];
+  }
+  __syncthreads();
+  // insert every pair's location; keep (entry, rank among the entry's pairs)
+  uint32_t ent[MERGE_PPT];
+  float wv[MERGE_PPT];
+#pragma unroll
+  for (int k = 0; k < MERGE_PPT; ++k) {
+    const int pidx = k * THREADS + t;
+    ent[k] = 0xFFFFFFFFu;
+    wv[k] = 0.0f;
+    if (pidx < nt * NB) {
+      const int32_t loc = S.a.pairs.loc[pidx];
+      wv[k] = S.a.pairs.w[pidx];
+      if (loc >= 0) {
+        uint32_t h = ((uint32_t)loc * 0x9E3779B1u) >> (32 - MERGE_HBITS);
+        while (true) {
+          const int32_t old = atomicCAS(&MW.tag[h], MERGE_EMPTY, loc);
+          if (old == MERGE_EMPTY || old == loc) break;
+          h = (h + 1) & (MERGE_H - 1);
+        }
+        const uint32_t sh = 16u * (h & 1u);
+        const uint32_t rank = (atomicAdd(&MW.cnt[h >> 1], 1u << sh) >> sh) & 0xFFFFu;
+        ent[k] = h | (rank << 16);
+      }
+    }
+  }
+  __syncthreads();
+  // exclusive scan over the entries: group index and first position of each
+  // occupied entry (this thread owns entries [t*HPT, (t+1)*HPT))
+  uint32_t c[MERGE_HPT];
+  uint32_t ng = 0, np = 0;
+#pragma unroll
+  for (int k = 0; k < MERGE_HPT / 2; ++k) {
+    const uint32_t wd = MW.cnt[t * (MERGE_HPT / 2) + k];
+    c[2 * k] = wd & 0xFFFFu;
+    c[2 * k + 1] = wd >> 16;
+  }
+#pragma unroll
+  for (int k = 0; k < MERGE_HPT; ++k) {
+    ng += c[k] ? 1u : 0u;
+    np += c[k];
+  }
+  uint32_t sg = ng, sp = np;  // inclusive scan inside the wave
+#pragma unroll
+  for (int off = 1; off < WAVE; off <<= 1) {
+    const uint32_t xg = __shfl_up(sg, off), xp = __shfl_up(sp, off);
+    if (lane >= off) {
+      sg += xg;
+      sp += xp;
+    }
+  }
+  if (lane == WAVE - 1) {
+    MW.wsum[wave][0] = sg;
+    MW.wsum[wave][1] = sp;
+  }
+  __syncthreads();
+  uint32_t gb = sg - ng, pb = sp - np;
+  for (int w = 0; w < wave; ++w) {
+    gb += MW.wsum[w][0];
+    pb += MW.wsum[w][1];
+  }
+  if (t == THREADS - 1) {
+    MW.ngroups = gb + ng;
+    S.a.grp.start[gb + ng] = (uint16_t)(pb + np);
+  }
+  uint32_t first[MERGE_HPT];
+#pragma unroll
+  for (int k = 0; k < MERGE_HPT; ++k) {
+    first[k] = pb;
+    if (c[k]) {
+      S.a.grp.loc[gb] = MW.tag[t * MERGE_HPT + k];
+      S.a.grp.start[gb] = (uint16_t)pb;
+      ++gb;
+      pb += c[k];
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < MERGE_HPT / 2; ++k) MW.cnt[t * (MERGE_HPT / 2) + k] = first[2 * k] | (first[2 * k + 1] << 16);
+  __syncthreads();
+  // pairs into group order (over the dead hash tags)
+  float* pw = reinterpret_cast<float*>(MW.tag);
+  uint8_t* pt = reinterpret_cast<uint8_t*>(MW.tag + MERGE_P);
+#pragma unroll
+  for (int k = 0; k < MERGE_PPT; ++k) {
+    if (ent[k] != 0xFFFFFFFFu) {
+      const uint32_t h = ent[k] & 0xFFFFu;
+      const uint32_t pos = ((MW.cnt[h >> 1] >> (16u * (h & 1u))) & 0xFFFFu) + (ent[k] >> 16);
+      pw[pos] = wv[k];
+      pt[pos] = (uint8_t)((k * THREADS + t) / NB);
+    }
+  }
+  __syncthreads();
+  // one row per distinct location: M lanes (lane = column) sum w * G over its pairs
+  constexpr int GROUPS = THREADS / M;
+  const int col = t % M;
+  const uint32_t ngroups = MW.ngroups;
+  for (uint32_t gi = t / M; gi < ngroups; gi += GROUPS) {
+    const uint32_t p0 = S.a.grp.start[gi], p1 = S.a.grp.start[gi + 1];
+    float acc = 0.0f;
+    for (uint32_t p = p0; p < p1; ++p) acc = fmaf(pw[p], MW.g[pt[p]][col], acc);
+    unsafeAtomicAdd(gtab + (size_t)S.a.grp.loc[gi] * M + col, acc);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Host side.
 
 thread_local int g_last_hip_error = 0;
@@ -1271,12 +1550,90 @@ size_t sort_ws_layout(int64_t L, SortWs* ws, char* base) {
   return off;
 }
 
+// Workspace of the batch-merged scatter for L lookups: the lookup sort (keys and
+// (lookup, 0) values, double-buffered).
+struct MergeWs {
+  SortWs sort;
+};
+
+size_t merge_ws_layout(int64_t L, MergeWs* ws, char* base) {
+  const int64_t n = L;
+  const int nblocks = (int)((n + SORT_TILE - 1) / SORT_TILE);
+  const int64_t nh = (int64_t)RADIX * nblocks;
+  const int64_t nbt = (nh + SCAN_TILE - 1) / SCAN_TILE;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    char* ptr = base ? base + off : nullptr;
+    off += align256(bytes);
+    return ptr;
+  };
+  char* k0 = take(n * 4);
+  char* k1 = take(n * 4);
+  char* v0 = take(n * 8);
+  char* v1 = take(n * 8);
+  char* h = take(nh * 4);
+  char* tt = take(nbt * 4);
+  if (ws) {
+    SortWs& so = ws->sort;
+    so.k0 = (uint32_t*)k0; so.k1 = (uint32_t*)k1; so.v0 = (uint2*)v0; so.v1 = (uint2*)v1;
+    so.hist = (uint32_t*)h; so.totals = (uint32_t*)tt;
+    so.n = n; so.nblocks = nblocks; so.nh = nh; so.nbt = nbt;
+  }
+  return off;
+}
+
+// Stable LSD radix sort of (key, value) pairs with keys in [0, N]; returns the
+// buffers holding the result.
+int radix_sort(const SortWs& ws, uint32_t N, hipStream_t s, uint32_t** kres, uint2** vres) {
+  int bits = 0;
+  while (bits < 32 && (N >> bits) != 0) ++bits;
+  uint32_t* kin = ws.k0;
+  uint32_t* kout = ws.k1;
+  uint2* vin = ws.v0;
+  uint2* vout = ws.v1;
+  for (int shift = 0; shift < bits; shift += RADIX_BITS) {
+    hipLaunchKernelGGL(k_radix_hist, dim3(ws.nblocks), dim3(THREADS), 0, s, kin, ws.n, shift, ws.hist, ws.nblocks);
+    hipLaunchKernelGGL(k_scan_blocks, dim3((unsigned)ws.nbt), dim3(THREADS), 0, s, ws.hist, ws.nh, ws.totals);
+    hipLaunchKernelGGL(k_scan_totals, dim3(1), dim3(THREADS), 0, s, ws.totals, ws.nbt);
+    hipLaunchKernelGGL(k_scan_add, dim3((unsigned)ws.nbt), dim3(THREADS), 0, s, ws.hist, ws.nh, ws.totals);
+    hipLaunchKernelGGL(k_radix_scatter, dim3(ws.nblocks), dim3(THREADS), 0, s, kin, vin, ws.n, shift, ws.hist,
+                       ws.nblocks, kout, vout);
+    if (int rc = launched()) return rc;
+    std::swap(kin, kout);
+    std::swap(vin, vout);
+  }
+  *kres = kin;
+  *vres = vin;
+  return LRAM_OK;
+}
+
 template <int DT, int M>
 struct BwdAtomicLaunch {
   static int go(const float* q, const Params& P, const void* table, const float* g, float* gt, float* gq,
                 hipStream_t s) {
-    hipLaunchKernelGGL((k_backward<DT, M, false>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g,
-                       gt, gq, (uint32_t*)nullptr, (uint2*)nullptr);
+    hipLaunchKernelGGL((k_backward<DT, M, false>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g, gt,
+                       gq, (uint32_t*)nullptr, (uint2*)nullptr);
+    return launched();
+  }
+};
+
+template <int DT, int M>
+struct BwdMergedLaunch {
+  static int go(const float* q, const Params& P, const void* table, const float* g, float* gt, float* gq,
+                const MergeWs& ws, hipStream_t s) {
+    if (!gt) return BwdAtomicLaunch<DT, M>::go(q, P, table, g, gt, gq, s);
+    hipLaunchKernelGGL(k_cell_key, dim3((unsigned)((P.L + THREADS - 1) / THREADS)), dim3(THREADS), 0, s, q, P,
+                       ws.sort.k0, ws.sort.v0);
+    if (int rc = launched()) return rc;
+    uint32_t* keys;
+    uint2* perm;
+    if (int rc = radix_sort(ws.sort, P.N, s, &keys, &perm)) return rc;
+    // one batch of at most MERGE_T lookups per workgroup
+    Params Pm = P;
+    Pm.lpw = P.lpw < MERGE_LPW ? P.lpw : MERGE_LPW;
+    const int64_t per_block = (int64_t)Pm.lpw * WAVES;
+    hipLaunchKernelGGL((k_backward_merged<DT, M>), dim3((unsigned)((P.L + per_block - 1) / per_block)),
+                       dim3(THREADS), 0, s, q, Pm, table, g, gt, gq, (const uint32_t*)keys, (const uint2*)perm);
     return launched();
   }
 };
@@ -1289,24 +1646,9 @@ struct BwdSortedLaunch {
                        gq, ws.k0, ws.v0);
     int rc = launched();
     if (rc || !gt) return rc;
-    int bits = 0;
-    while (bits < 32 && (P.N >> bits) != 0) ++bits;  // keys lie in [0, N]
-    uint32_t* kin = ws.k0;
-    uint32_t* kout = ws.k1;
-    uint2* vin = ws.v0;
-    uint2* vout = ws.v1;
-    for (int shift = 0; shift < bits; shift += RADIX_BITS) {
-      hipLaunchKernelGGL(k_radix_hist, dim3(ws.nblocks), dim3(THREADS), 0, s, kin, ws.n, shift, ws.hist,
-                         ws.nblocks);
-      hipLaunchKernelGGL(k_scan_blocks, dim3((unsigned)ws.nbt), dim3(THREADS), 0, s, ws.hist, ws.nh, ws.totals);
-      hipLaunchKernelGGL(k_scan_totals, dim3(1), dim3(THREADS), 0, s, ws.totals, ws.nbt);
-      hipLaunchKernelGGL(k_scan_add, dim3((unsigned)ws.nbt), dim3(THREADS), 0, s, ws.hist, ws.nh, ws.totals);
-      hipLaunchKernelGGL(k_radix_scatter, dim3(ws.nblocks), dim3(THREADS), 0, s, kin, vin, ws.n, shift, ws.hist,
-                         ws.nblocks, kout, vout);
-      if ((rc = launched())) return rc;
-      std::swap(kin, kout);
-      std::swap(vin, vout);
-    }
+    uint32_t* kin;
+    uint2* vin;
+    if ((rc = radix_sort(ws, P.N, s, &kin, &vin))) return rc;  // keys lie in [0, N]
     // span: 256 pairs per group, fewer when that would leave CUs idle (about
     // 32 groups per CU for 256 CUs)
     int64_t span = (ws.n + 256 * 32 - 1) / (256 * 32);
@@ -1329,7 +1671,7 @@ const char* lram_strerror(int status) {
   switch (status) {
     case LRAM_OK: return "ok";
     case LRAM_EINVAL: return "invalid argument (null/misaligned pointer or negative size)";
-    case LRAM_EBADK: return "invalid torus: every K_i must be even and >= 2, N = prod K_i < 2^31";
+    case LRAM_EBADK: return "invalid torus: every K_i must be even, 2 <= K_i <= 8192, N = prod K_i < 2^31";
     case LRAM_EDTYPE: return "unsupported table dtype or value dimension m";
     case LRAM_EWORKSPACE: return "workspace missing or too small";
     case LRAM_EMODE: return "unknown scatter mode";
@@ -1365,16 +1707,25 @@ int lram_forward(const float* q, int64_t B, int64_t H, const int32_t K[8], const
   return dispatch<FwdLaunch>(dtype, m, q, P, table, out, (hipStream_t)stream);
 }
 
+int lram_scatter_mode_resolved(int64_t B, int64_t H, int mode, int* resolved) {
+  if (!resolved || B < 0 || H < 0 || (H != 0 && B > INT64_MAX / H)) return LRAM_EINVAL;
+  if (mode < LRAM_SCATTER_ATOMIC || mode > LRAM_SCATTER_AUTO) return LRAM_EMODE;
+  *resolved = mode != LRAM_SCATTER_AUTO ? mode : (B * H >= AUTO_MERGE_MIN ? LRAM_SCATTER_MERGED : LRAM_SCATTER_ATOMIC);
+  return LRAM_OK;
+}
+
 int lram_backward_workspace_bytes(int64_t B, int64_t H, int32_t m, int mode, size_t* bytes) {
   if (!bytes || B < 0 || H < 0) return LRAM_EINVAL;
   if (m != 32 && m != 64) return LRAM_EDTYPE;
+  if (int rc = lram_scatter_mode_resolved(B, H, mode, &mode)) return rc;
   if (mode == LRAM_SCATTER_ATOMIC) {
     *bytes = 0;
     return LRAM_OK;
   }
-  if (mode == LRAM_SCATTER_SORTED) {
+  if (mode == LRAM_SCATTER_SORTED || mode == LRAM_SCATTER_MERGED) {
     if (H != 0 && B > INT64_MAX / H / NB) return LRAM_EINVAL;
-    *bytes = sort_ws_layout(B * H, nullptr, nullptr);
+    *bytes = mode == LRAM_SCATTER_SORTED ? sort_ws_layout(B * H, nullptr, nullptr)
+                                         : merge_ws_layout(B * H, nullptr, nullptr);
     return LRAM_OK;
   }
   return LRAM_EMODE;
@@ -1391,7 +1742,7 @@ int lram_backward(const float* q, int64_t B, int64_t H, const int32_t K[8], cons
   if (rc) return rc;
   rc = check_table(table, dtype, N, m, P, L);
   if (rc) return rc;
-  if (mode != LRAM_SCATTER_ATOMIC && mode != LRAM_SCATTER_SORTED) return LRAM_EMODE;
+  if (int rc2 = lram_scatter_mode_resolved(B, H, mode, &mode)) return rc2;
   if (L == 0) return LRAM_OK;
   if (!grad_out || (reinterpret_cast<uintptr_t>(grad_out) & 15)) return LRAM_EINVAL;
   if (!grad_table && !grad_q) return LRAM_EINVAL;
@@ -1399,6 +1750,13 @@ int lram_backward(const float* q, int64_t B, int64_t H, const int32_t K[8], cons
   if (mode == LRAM_SCATTER_ATOMIC)
     return dispatch<BwdAtomicLaunch>(dtype, m, q, P, table, grad_out, grad_table, grad_q, (hipStream_t)stream);
   if (L > INT64_MAX / NB || L * NB >= (int64_t(1) << 32)) return LRAM_EINVAL;  // positions are 32-bit
+  if (mode == LRAM_SCATTER_MERGED) {
+    const size_t need = merge_ws_layout(L, nullptr, nullptr);
+    if (!workspace || ws_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LRAM_EWORKSPACE;
+    MergeWs ws;
+    merge_ws_layout(L, &ws, reinterpret_cast<char*>(workspace));
+    return dispatch<BwdMergedLaunch>(dtype, m, q, P, table, grad_out, grad_table, grad_q, ws, (hipStream_t)stream);
+  }
   const size_t need = sort_ws_layout(L, nullptr, nullptr);
   if (!workspace || ws_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LRAM_EWORKSPACE;
   SortWs ws;

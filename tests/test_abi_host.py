@@ -58,6 +58,8 @@ def test_forward_validation(lib):
     assert _fwd(lib, K=(ctypes.c_int32 * 8)(*([0] + [4] * 7))) == 2          # K < 2
     assert _fwd(lib, K=(ctypes.c_int32 * 8)(*([16] * 8))) == 2                # N >= 2^31
     assert _fwd(lib, N=12345) == 2                                            # N != prod K
+    big = (ctypes.c_int32 * 8)(*([8194, 2, 2, 2, 2, 2, 2, 2]))
+    assert _fwd(lib, K=big, N=8194 * 128) == 2                                # K_i > 8192
     assert _fwd(lib, dtype=7) == 3
     assert _fwd(lib, m=48) == 3
     assert _fwd(lib, q=None) == 1
@@ -89,7 +91,22 @@ def test_backward_validation(lib):
     assert lib.lram_backward_workspace_bytes(4, 1, 32, 9, ctypes.byref(n)) == 5
     assert lib.lram_backward_workspace_bytes(4, 1, 32, 1, ctypes.byref(n)) == 0 and n.value >= 4 * 32 * 24
     assert bwd(mode=1, ws=None) == 4  # sorted mode without a workspace
+    assert lib.lram_backward_workspace_bytes(4, 1, 32, 2, ctypes.byref(n)) == 0 and n.value >= 4 * 24
+    assert bwd(mode=2, ws=None) == 4  # merged mode without a workspace
+    assert bwd(mode=2, ws=FAKE_MIS, wsb=1 << 20) == 4  # misaligned workspace
     assert lib.lram_backward_workspace_bytes(4, 1, 48, 0, ctypes.byref(n)) == 3
+
+
+def test_auto_mode(lib):
+    r = ctypes.c_int(-1)
+    assert lib.lram_scatter_mode_resolved(4, 1, 3, ctypes.byref(r)) == 0 and r.value == 0        # small: atomic
+    assert lib.lram_scatter_mode_resolved(8192, 16, 3, ctypes.byref(r)) == 0 and r.value == 2    # 131072: merged
+    assert lib.lram_scatter_mode_resolved(8192, 16, 1, ctypes.byref(r)) == 0 and r.value == 1    # explicit kept
+    assert lib.lram_scatter_mode_resolved(4, 1, 4, ctypes.byref(r)) == 5
+    assert lib.lram_scatter_mode_resolved(-1, 1, 0, ctypes.byref(r)) == 1
+    n = ctypes.c_size_t(1)
+    assert lib.lram_backward_workspace_bytes(4, 1, 32, 3, ctypes.byref(n)) == 0 and n.value == 0
+    assert lib.lram_backward_workspace_bytes(8192, 16, 32, 3, ctypes.byref(n)) == 0 and n.value >= 131072 * 24
 
 
 def test_no_oracle_in_product():

@@ -135,7 +135,7 @@ def _tol(dtype):
     return 1e-5 if dtype == torch.float32 else 2e-2
 
 
-@pytest.mark.parametrize("mode", ["atomic", "sorted"])
+@pytest.mark.parametrize("mode", ["atomic", "sorted", "merged"])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("m", [32, 64])
 @pytest.mark.parametrize("K", [(4,) * 8, (2, 4, 6, 8, 2, 4, 6, 8)])
@@ -173,21 +173,25 @@ def test_forward_backward_small(K, m, dtype, mode):
     assert np.all(out.float().cpu().numpy()[10] == 0) and np.all(gq.cpu().numpy()[10] == 0)
 
 
-def test_backward_accumulates():
+@pytest.mark.parametrize("mode", ["atomic", "sorted", "merged"])
+def test_backward_accumulates(mode):
     K = (4,) * 8
     rng = np.random.default_rng(12)
     q = torch.from_numpy((rng.random((500, 8)) * 4).astype(np.float32)).to(DEV)
     table = _small_table(K, 32, torch.float32)
     G = torch.randn((500, 32), device=DEV)
-    gt1, _ = lram.backward(q, table, K, G)
+    gt1, gq1 = lram.backward(q, table, K, G, mode=mode)
     gt2 = gt1.clone()
-    lram.backward(q, table, K, G, grad_table=gt2, want_grad_q=False)
+    lram.backward(q, table, K, G, grad_table=gt2, want_grad_q=False, mode=mode)
+    # dq alone (no value gradient) is the same in every mode
+    _, gq3 = lram.backward(q, table, K, G, grad_table=False, mode=mode)
     torch.cuda.synchronize()
+    assert torch.equal(gq1, gq3)
     # atomic accumulation order varies between calls: compare at the fp32 parity bar
     np.testing.assert_allclose(gt2.cpu().numpy(), 2 * gt1.cpu().numpy(), rtol=1e-5, atol=1e-7)
 
 
-@pytest.mark.parametrize("mode", ["atomic", "sorted"])
+@pytest.mark.parametrize("mode", ["atomic", "sorted", "merged"])
 @pytest.mark.parametrize("name", ["k4-m32-f32-uniform", "k4-m32-f32-gmm64"])
 def test_workload_full_parity(name, mode):
     """Small workloads in full: every lookup, every output."""
@@ -214,7 +218,7 @@ def test_workload_full_parity(name, mode):
     assert np.all(dV[mask] == 0)
 
 
-@pytest.mark.parametrize("mode", ["atomic", "sorted"])
+@pytest.mark.parametrize("mode", ["atomic", "sorted", "merged"])
 def test_hot_rows(mode):
     """Many lookups on a few lattice cells: runs of one location span many
     64-pair chunks of the sorted reduction (and contend in the atomic one)."""
@@ -222,7 +226,7 @@ def test_hot_rows(mode):
     K = (8,) * 8
     rng = np.random.default_rng(13)
     centres = (rng.random((3, 8)) * 8)
-    L = 20000
+    L = 70001  # enough lookups for full 64-lookup merge batches, and a ragged last one
     q_np = (centres[rng.integers(0, 3, L)] + 0.05 * rng.standard_normal((L, 8))).astype(np.float32)
     q = torch.from_numpy(q_np).to(DEV)
     table = _small_table(K, 32, torch.float32)
@@ -241,13 +245,43 @@ def test_hot_rows(mode):
     assert _rel_rows(gq.cpu().numpy(), oracle.grad_query(nb, rows, G.cpu().numpy())).max() <= 1e-4
 
 
-def test_sorted_workspace_errors():
+def test_mixed_batches_merged():
+    """Merged scatter on a batch whose sorted order holds both clustered runs
+    (merged in LDS) and thinly spread lookups (direct atomics), with full
+    64-lookup batches and a ragged last one."""
+    _say("mixed batches merged")
+    K = (8,) * 8
+    rng = np.random.default_rng(14)
+    centres = rng.random((5, 8)) * 8
+    L = 90003
+    q_np = (rng.random((L, 8)) * 8).astype(np.float32)
+    hot = rng.random(L) < 0.5
+    q_np[hot] = np.mod(centres[rng.integers(0, 5, hot.sum())] + 0.2 * rng.standard_normal((hot.sum(), 8)),
+                       8).astype(np.float32)
+    q = torch.from_numpy(q_np).to(DEV)
+    table = _small_table(K, 32, torch.bfloat16)
+    G = torch.randn((L, 32), device=DEV)
+    gt, gq = lram.backward(q, table, K, G, mode="merged")
+    gta, gqa = lram.backward(q, table, K, G, mode="atomic")
+    torch.cuda.synchronize()
+    assert torch.equal(gq, gqa)  # dq does not depend on the scatter
+    nb = oracle.neighbors(q_np, K)
+    uniq, acc = oracle.grad_table_rows(nb, G.cpu().numpy())
+    dV = gt.cpu().numpy()
+    assert _rel_rows(dV[uniq], acc).max() <= 1e-5
+    mask = np.ones(dV.shape[0], bool)
+    mask[uniq] = False
+    assert np.all(dV[mask] == 0)
+
+
+@pytest.mark.parametrize("mode", ["sorted", "merged"])
+def test_workspace_errors(mode):
     K = (4,) * 8
     q = torch.rand((100, 8), device=DEV) * 4
     table = _small_table(K, 32, torch.float32)
     G = torch.randn((100, 32), device=DEV)
-    need = lram.backward_workspace_bytes(100, 1, 32, "sorted")
-    assert need > 100 * 32 * 24
+    need = lram.backward_workspace_bytes(100, 1, 32, mode)
+    assert need > 100 * 24
     small = torch.empty(need - 256, dtype=torch.uint8, device=DEV)
     with pytest.raises(lram.LramError):
-        lram.backward(q, table, K, G, mode="sorted", workspace=small)
+        lram.backward(q, table, K, G, mode=mode, workspace=small)
