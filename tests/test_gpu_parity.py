@@ -3,8 +3,11 @@
 Bars (fixed before any kernel ran):
   * neighbour locations: bit-exact, in selection order; recipe distances and
     recipe weights: bit-exact (they are decided in the same fp32 arithmetic);
-  * forward and both gradients, per output row: relative L2 error <= 1e-5 for
-    fp32 tables and <= 2e-2 for bf16 tables, against the fp64 oracle;
+  * forward, per output row: relative L2 error <= 1e-5 for fp32 tables and
+    <= 2e-2 for bf16 tables (the output is rounded to bf16 once), against the
+    fp64 oracle;
+  * dq and the value-gradient rows (fp32 outputs for either table dtype, whose
+    bf16 entries are exact in fp32): relative L2 error <= 1e-5;
   * value-gradient rows no lookup touched stay exactly 0.
 """
 import numpy as np
@@ -162,7 +165,7 @@ def test_forward_backward_small(K, m, dtype, mode):
     Gn = G.cpu().numpy()
     dq_ref = oracle.grad_query(nb, rows, Gn)
     err = _rel_rows(gq.cpu().numpy(), dq_ref)
-    assert err.max() <= (1e-4 if dtype == torch.float32 else 2e-2), err.max()
+    assert err.max() <= 1e-5, err.max()
     dV_ref = oracle.grad_table_dense(nb, Gn, int(np.prod(K)))
     dV = gt.cpu().numpy()
     touched = np.unique(nb["slot"][nb["slot"] >= 0])
@@ -209,7 +212,7 @@ def test_workload_full_parity(name, mode):
     assert _rel_rows(out.cpu().numpy().reshape(w.L, -1), oracle.forward(nb, rows).reshape(w.L, -1)).max() <= 1e-5
     Gn = G.cpu().numpy()
     dq_ref = oracle.grad_query(nb, rows, Gn)
-    assert _rel_rows(gq.cpu().numpy().reshape(w.L, -1), dq_ref.reshape(w.L, -1)).max() <= 1e-4
+    assert _rel_rows(gq.cpu().numpy().reshape(w.L, -1), dq_ref.reshape(w.L, -1)).max() <= 1e-5
     uniq, acc = oracle.grad_table_rows(nb, Gn)
     dV = gt.cpu().numpy()
     assert _rel_rows(dV[uniq], acc).max() <= 1e-5
@@ -242,7 +245,7 @@ def test_hot_rows(mode):
     mask[uniq] = False
     assert np.all(dV[mask] == 0)
     rows = oracle.gather_rows(table.cpu().numpy(), nb["slot"])
-    assert _rel_rows(gq.cpu().numpy(), oracle.grad_query(nb, rows, G.cpu().numpy())).max() <= 1e-4
+    assert _rel_rows(gq.cpu().numpy(), oracle.grad_query(nb, rows, G.cpu().numpy())).max() <= 1e-5
 
 
 def test_mixed_batches_merged():
