@@ -21,6 +21,11 @@ Lattices"):
   being dx/dq), with the selection held fixed (Sec. 2.6: the kernel returns
   the weights and their partial derivatives for an autograd wrapper).
 
+* ``theta_*``    -- the activation layer of Sec. 2.3 in front of the lookup:
+  theta(z) = (sum_i 1/|z_i|)^-1 phi_32((K_i / 2 pi) arg z_i) for z in C^8,
+  given as 16 reals (Re z_0, Im z_0, ..., Re z_7, Im z_7), and its gradients
+  with respect to z (through arg and the scale) and to the value table.
+
 Scale and the other readings of the paper are stated in the header of
 ``lram_oracle.c``.  All functions take numpy arrays on the host.
 """
@@ -182,4 +187,70 @@ def grad_table_dense(nb: dict, G: np.ndarray, N: int) -> np.ndarray:
     uniq, acc = grad_table_rows(nb, G)
     out = np.zeros((N, acc.shape[1] if acc.ndim == 2 else np.asarray(G).shape[-1]), np.float64)
     out[uniq] = acc
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Activation layer (Sec. 2.3).
+
+def theta_coords(z: np.ndarray, K):
+    """Torus coordinates and output scale of theta for z[..., 16] (Sec. 2.3).
+
+    q_i = (K_i / (2 pi)) * arg z_i, formed in fp64 and rounded once to fp32
+    (the query precision of the lookup); s = (sum_i 1/|z_i|)^-1 in fp64 -- the
+    displayed formula of Sec. 2.3, which the text calls a harmonic mean
+    (without its factor n).  A zero z_i gives s = 0 (the continuous
+    extension); a non-finite input gives a NaN query (empty neighbour list)
+    and s = 0.
+    """
+    K = _check_k(K)
+    z = np.asarray(np.asarray(z, np.float32), np.float64)
+    assert z.shape[-1] == 16
+    a, b = z[..., 0::2], z[..., 1::2]
+    c = K.astype(np.float64) / (2.0 * np.pi)
+    finite = np.all(np.isfinite(z), axis=-1)
+    with np.errstate(divide="ignore", invalid="ignore", over="ignore"):
+        q = (np.arctan2(b, a) * c).astype(np.float32)
+        s = 1.0 / np.sum(1.0 / np.hypot(a, b), axis=-1)
+    q = np.where(finite[..., None], q, np.float32(np.nan))
+    s = np.where(finite, s, 0.0)
+    return q, s
+
+
+def theta_forward(nb: dict, rows: np.ndarray, s: np.ndarray) -> np.ndarray:
+    """theta = s * phi_32(q), fp64 (nb and rows of the queries from theta_coords)."""
+    return np.asarray(s, np.float64)[..., None] * forward(nb, rows)
+
+
+def theta_grad_table_rows(nb: dict, s: np.ndarray, G: np.ndarray):
+    """Value-table gradient of <G, theta>: the lookup's with G scaled by s."""
+    return grad_table_rows(nb, np.asarray(G, np.float64) * np.asarray(s, np.float64)[..., None])
+
+
+def theta_grad_z(z: np.ndarray, K, nb: dict, rows: np.ndarray, s: np.ndarray, G: np.ndarray) -> np.ndarray:
+    """d<G, theta>/dz[..., 16] (selection held fixed), fp64.
+
+    With r_i = |z_i|, t_i = arg z_i, q_i = c_i t_i, c_i = K_i / (2 pi):
+    ds/da_i = s^2 a_i / r_i^3, ds/db_i = s^2 b_i / r_i^3 (from s = 1 / sum 1/r),
+    dt_i/da_i = -b_i / r_i^2, dt_i/db_i = a_i / r_i^2, and
+    d<G, theta>/ds = <G, phi>, d<G, theta>/dq = s * (dq of the lookup for G).
+    Zero where s = 0 (a zero or non-finite entry).
+    """
+    K = _check_k(K)
+    z = np.asarray(np.asarray(z, np.float32), np.float64)
+    a, b = z[..., 0::2], z[..., 1::2]
+    c = K.astype(np.float64) / (2.0 * np.pi)
+    s = np.asarray(s, np.float64)
+    G = np.asarray(G, np.float64)
+    dLds = np.einsum("...m,...m->...", G, forward(nb, rows))
+    dLdq = s[..., None] * grad_query(nb, rows, G)
+    ok = s > 0
+    with np.errstate(divide="ignore", invalid="ignore"):
+        r2 = a * a + b * b
+        r3 = r2 * np.sqrt(r2)
+        ga = dLds[..., None] * s[..., None] ** 2 * a / r3 - dLdq * c * b / r2
+        gb = dLds[..., None] * s[..., None] ** 2 * b / r3 + dLdq * c * a / r2
+    out = np.empty(z.shape, np.float64)
+    out[..., 0::2] = np.where(ok[..., None], ga, 0.0)
+    out[..., 1::2] = np.where(ok[..., None], gb, 0.0)
     return out
