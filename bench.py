@@ -115,7 +115,8 @@ def main():
     ap.add_argument("--mode", default="auto", choices=["auto", "atomic", "sorted", "merged"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-compare", action="store_true", help="skip timing the other scatter mode")
+    ap.add_argument("--no-compare", action="store_true", help="skip timing the other scatter modes")
+    ap.add_argument("--no-theta", action="store_true", help="skip timing the activation layer path")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (HBM counter calibration)")
     args = ap.parse_args()
@@ -211,6 +212,33 @@ def main():
         del ws
         log("backward with the %s scatter: %.3f ms" % (other, by_scatter[other]))
 
+    # the activation layer of Sec. 2.3 in front of the same lookups (not part of `value`)
+    theta = None
+    if not args.no_theta:
+        z = torch.from_numpy(W.theta_inputs(w)).to(dev)
+        gz = torch.empty_like(z)
+        nbytes = lram.backward_workspace_bytes(w.B, w.H, w.m, mode)
+        wsp = torch.empty(nbytes, dtype=torch.uint8, device=dev) if nbytes else None
+        lram.theta_forward(z, table, w.K, out=out)
+        lram.theta_backward(z, table, w.K, G, grad_table=gtab, grad_z=gz, mode=mode, workspace=wsp)
+        torch.cuda.synchronize()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        tf = tb = 0.0
+        for _ in range(5):
+            e[0].record(stream)
+            lram.theta_forward(z, table, w.K, out=out)
+            e[1].record(stream)
+            lram.theta_backward(z, table, w.K, G, grad_table=gtab, grad_z=gz, mode=mode, workspace=wsp)
+            e[2].record(stream)
+            torch.cuda.synchronize()
+            tf += e[0].elapsed_time(e[1]) / 5
+            tb += e[1].elapsed_time(e[2]) / 5
+        theta = {"fwd_ms": tf, "bwd_ms": tb, "lookups_per_s": w.L / ((tf + tb) * 1e-3),
+                 "fwd_lookups_per_s": w.L / (tf * 1e-3), "scatter": mode,
+                 "input": "z [B, H, 16]: the workload's queries as arguments, Rayleigh moduli"}
+        log("activation layer + lookup: forward %.3f ms, backward %.3f ms" % (tf, tb))
+        del z, gz, wsp
+
     st = 4 if w.dtype == "f32" else 2
     L = w.L
     fwd_bytes = L * (32 + w.m * st) + U * w.m * st
@@ -247,6 +275,7 @@ def main():
         "bwd_ms": bwd_ms,
         "bwd_ms_by_scatter": by_scatter,
         "distinct_rows": U,
+        "theta": theta,
         "roofline": {"kernel": kname, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "bytes_per_launch": kbytes, "requested_bytes_per_launch": kreq,

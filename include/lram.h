@@ -138,6 +138,46 @@ int lram_backward(const float* q, int64_t B, int64_t H, const int32_t K[8], cons
                   int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_q, int mode,
                   void* workspace, size_t ws_bytes, void* stream);
 
+/*
+ * Activation layer in front of the lookup (Sec. 2.3).  Each lookup takes 8
+ * complex numbers z_i = z[l][2i] + i z[l][2i+1] (z is [L][16] fp32, 16-byte
+ * aligned) and computes
+ *
+ *     theta(z) = (sum_i 1/|z_i|)^-1 phi(q),   q_i = (K_i / 2 pi) arg z_i,
+ *
+ * the scale being the displayed formula of Sec. 2.3 (the text calls it a
+ * harmonic mean; the formula has no factor 8), so theta(lambda z) =
+ * lambda theta(z) for lambda >= 0.  q_i is formed in fp64 (atan2 of the fp32
+ * inputs times K_i / 2 pi) and rounded once to fp32; the lookup then proceeds
+ * exactly as lram_forward on that q.  A zero z_i gives scale 0 (output 0,
+ * gradients 0: the continuous extension); a non-finite input gives output 0
+ * and zero gradients.
+ */
+
+/* lram_theta_coords -- q [L][8] fp32 and scale s [L] fp32 (nullable) as the
+ * activation layer computes them (parity surface). */
+int lram_theta_coords(const float* z, int64_t B, int64_t H, const int32_t K[8], float* q, float* s, void* stream);
+
+/* lram_theta_forward -- out[l] = theta(z_l) in the table dtype (fp32
+ * accumulation, the scale folded into the 32 weights, one rounding). */
+int lram_theta_forward(const float* z, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
+                       int64_t N, int32_t m, void* out, void* stream);
+
+/*
+ * lram_theta_backward -- gradients of sum_l <grad_out[l], theta(z_l)>, selection
+ * held fixed:
+ *   grad_table[s] += sum over (l, j) with slot_j(l) = s of scale_l w_j grad_out[l]
+ *       (accumulated; same modes, workspace and rules as lram_backward, whose
+ *        lram_backward_workspace_bytes applies unchanged)
+ *   grad_z[l] [16] fp32 (overwritten; nullable): with r_i = |z_i|, c_i = K_i/2pi,
+ *       dL/ds = sum_j w_j <G, v_j>, dL/dq = s dq (dq as in lram_backward),
+ *       dL/dRe z_i = dL/ds s^2 Re z_i / r_i^3 - dL/dq_i c_i Im z_i / r_i^2,
+ *       dL/dIm z_i = dL/ds s^2 Im z_i / r_i^3 + dL/dq_i c_i Re z_i / r_i^2.
+ */
+int lram_theta_backward(const float* z, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
+                        int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_z, int mode,
+                        void* workspace, size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

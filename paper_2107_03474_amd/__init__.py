@@ -21,7 +21,8 @@ import torch  # noqa: F401  -- loads the HIP runtime liblram.so must share
 
 __all__ = ["neighbors", "forward", "backward", "backward_workspace_bytes", "lookup", "LramLookup",
            "library_path", "load", "LramError", "F32", "BF16", "SCATTER_ATOMIC", "SCATTER_SORTED",
-           "SCATTER_MERGED", "SCATTER_AUTO", "resolved_mode", "NB"]
+           "SCATTER_MERGED", "SCATTER_AUTO", "resolved_mode", "NB",
+           "theta_coords", "theta_forward", "theta_backward", "ThetaLookup", "theta"]
 
 NB = 32
 F32, BF16 = 0, 1
@@ -66,6 +67,12 @@ def load():
             lib.lram_scatter_mode_resolved.restype = I
             lib.lram_backward.argtypes = [P, I64, I64, P, P, I, I64, I32, P, P, P, I, P, ctypes.c_size_t, P]
             lib.lram_backward.restype = I
+            lib.lram_theta_coords.argtypes = [P, I64, I64, P, P, P, P]
+            lib.lram_theta_coords.restype = I
+            lib.lram_theta_forward.argtypes = [P, I64, I64, P, P, I, I64, I32, P, P]
+            lib.lram_theta_forward.restype = I
+            lib.lram_theta_backward.argtypes = [P, I64, I64, P, P, I, I64, I32, P, P, P, I, P, ctypes.c_size_t, P]
+            lib.lram_theta_backward.restype = I
             _lib = lib
     return _lib
 
@@ -108,12 +115,12 @@ def _table_dtype(table: torch.Tensor) -> int:
     raise LramError("table must be float32 or bfloat16")
 
 
-def _bh(q: torch.Tensor) -> Tuple[int, int]:
+def _bh(q: torch.Tensor, last: int = 8, name: str = "q") -> Tuple[int, int]:
+    if q.dim() not in (2, 3) or q.shape[-1] != last:
+        raise LramError("%s must be [B, H, %d] or [L, %d]" % (name, last, last))
     if q.dim() == 2:
         return q.shape[0], 1
-    if q.dim() == 3:
-        return q.shape[0], q.shape[1]
-    raise LramError("q must be [B, H, 8] or [L, 8]")
+    return q.shape[0], q.shape[1]
 
 
 def neighbors(q: torch.Tensor, K: Sequence[int], want_d2: bool = True):
@@ -204,3 +211,77 @@ class LramLookup(torch.autograd.Function):
 
 def lookup(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], mode="auto") -> torch.Tensor:
     return LramLookup.apply(q, table, tuple(K), mode)
+
+
+# ---------------------------------------------------------------------------
+# Activation layer (Sec. 2.3): z [..., 16] = 8 complex numbers (Re, Im) per head.
+
+def theta_coords(z: torch.Tensor, K: Sequence[int]):
+    """(q [..., 8] fp32, s [...] fp32): torus coordinates and output scale of theta."""
+    lib = load()
+    B, H = _bh(z, 16, "z")
+    q = torch.empty(z.shape[:-1] + (8,), dtype=torch.float32, device=z.device)
+    sc = torch.empty(z.shape[:-1], dtype=torch.float32, device=z.device)
+    _check(lib.lram_theta_coords(_dev(z, "z", torch.float32), B, H, _K(K), _dev(q, "q"), _dev(sc, "s"), _stream(z)))
+    return q, sc
+
+
+def theta_forward(z: torch.Tensor, table: torch.Tensor, K: Sequence[int], out: Optional[torch.Tensor] = None):
+    """theta(z) = (sum 1/|z_i|)^-1 phi((K_i / 2 pi) arg z_i): [..., m] in the table dtype."""
+    lib = load()
+    B, H = _bh(z, 16, "z")
+    N, m = table.shape
+    if out is None:
+        out = torch.empty(z.shape[:-1] + (m,), dtype=table.dtype, device=z.device)
+    _check(lib.lram_theta_forward(_dev(z, "z", torch.float32), B, H, _K(K), _dev(table, "table"),
+                                  _table_dtype(table), N, m, _dev(out, "out", table.dtype), _stream(z)))
+    return out
+
+
+def theta_backward(z: torch.Tensor, table: torch.Tensor, K: Sequence[int], grad_out: torch.Tensor,
+                   grad_table: Optional[torch.Tensor] = None, want_grad_z: bool = True, mode="auto",
+                   workspace: Optional[torch.Tensor] = None, grad_z: Optional[torch.Tensor] = None):
+    """Gradients of <grad_out, theta(z)>: grad_table [N, m] fp32 ACCUMULATED into
+    (allocated zeroed if None, False to skip), grad_z [..., 16] fp32."""
+    lib = load()
+    B, H = _bh(z, 16, "z")
+    N, m = table.shape
+    if grad_table is None:
+        grad_table = torch.zeros((N, m), dtype=torch.float32, device=z.device)
+    gz = None
+    if want_grad_z:
+        gz = grad_z if grad_z is not None else torch.empty(z.shape, dtype=torch.float32, device=z.device)
+    mode_i = _MODES[mode]
+    ws_bytes = backward_workspace_bytes(B, H, m, mode_i)
+    if ws_bytes and workspace is None:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=z.device)
+    gt_ptr = _dev(grad_table, "grad_table", torch.float32) if grad_table is not False else None
+    _check(lib.lram_theta_backward(_dev(z, "z", torch.float32), B, H, _K(K), _dev(table, "table"),
+                                   _table_dtype(table), N, m, _dev(grad_out, "grad_out", torch.float32), gt_ptr,
+                                   _dev(gz, "grad_z") if gz is not None else None, mode_i,
+                                   _dev(workspace, "workspace") if workspace is not None else None,
+                                   workspace.numel() if workspace is not None else 0, _stream(z)))
+    return (grad_table if grad_table is not False else None), gz
+
+
+class ThetaLookup(torch.autograd.Function):
+    """Autograd wrapper of the activation layer + lookup: dz and a dense dtable."""
+
+    @staticmethod
+    def forward(ctx, z, table, K, mode):
+        ctx.save_for_backward(z, table)
+        ctx.K = tuple(int(k) for k in K)
+        ctx.mode = mode
+        return theta_forward(z.contiguous(), table.contiguous(), ctx.K)
+
+    @staticmethod
+    def backward(ctx, g):
+        z, table = ctx.saved_tensors
+        g32 = g.contiguous().to(torch.float32)
+        gt, gz = theta_backward(z, table, ctx.K, g32, grad_table=None if ctx.needs_input_grad[1] else False,
+                                want_grad_z=ctx.needs_input_grad[0], mode=ctx.mode)
+        return gz, (gt.to(table.dtype) if gt is not None else None), None, None
+
+
+def theta(z: torch.Tensor, table: torch.Tensor, K: Sequence[int], mode="auto") -> torch.Tensor:
+    return ThetaLookup.apply(z, table, tuple(K), mode)

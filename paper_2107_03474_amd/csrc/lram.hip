@@ -61,6 +61,7 @@ struct Params {
   uint32_t N;
   int32_t lpw;       // lookups per wave (1..64)
   int64_t L;
+  double cK[8];      // K_i / (2 pi): torus coordinate per radian of arg z_i (activation layer)
 };
 
 // Per-lookup frame written by phase A (96 bytes).
@@ -69,7 +70,8 @@ struct alignas(16) Frame {
   uint32_t sel[8];    // v_perm selector of original coordinate i: byte r_i (its F position) into byte 0
   int16_t c[8];       // closest lattice point
   uint32_t misc;      // bits 0-7: sign flips s'_i = -1; bit 8: query finite
-  uint32_t pad[3];
+  float s;            // output scale: 1, or (sum 1/|z_i|)^-1 behind the activation layer
+  uint32_t pad[2];
 };
 
 // A selected neighbour as handed from the search to the gather / scatter.
@@ -160,15 +162,47 @@ __device__ __forceinline__ void d8_round(const float (&y)[8], int (&r)[8]) {
   }
 }
 
+// The query of one lookup and its output scale.  TH = false: q itself
+// (8 floats), scale 1.  TH = true, the activation layer of Sec. 2.3: z_i =
+// in[2i] + i in[2i+1], q_i = (K_i / 2 pi) arg z_i formed in fp64 and rounded
+// once to fp32, scale (sum_i 1/|z_i|)^-1 (0 when some z_i = 0); a non-finite
+// input gives a NaN query (empty neighbour list) and scale 0.
+template <bool TH>
+__device__ __forceinline__ void load_query(const float* __restrict__ in, const Params P, float (&qq)[8],
+                                           float& scale) {
+  if constexpr (!TH) {
+    const float4 a = reinterpret_cast<const float4*>(in)[0];
+    const float4 b = reinterpret_cast<const float4*>(in)[1];
+    qq[0] = a.x; qq[1] = a.y; qq[2] = a.z; qq[3] = a.w;
+    qq[4] = b.x; qq[5] = b.y; qq[6] = b.z; qq[7] = b.w;
+    scale = 1.0f;
+  } else {
+    float z[16];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const float4 v = reinterpret_cast<const float4*>(in)[k];
+      z[4 * k] = v.x; z[4 * k + 1] = v.y; z[4 * k + 2] = v.z; z[4 * k + 3] = v.w;
+    }
+    bool finite = true;
+    double inv = 0.0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const double a = z[2 * i], b = z[2 * i + 1];
+      finite = finite && isfinite(z[2 * i]) && isfinite(z[2 * i + 1]);
+      inv += 1.0 / sqrt(a * a + b * b);
+      qq[i] = (float)(atan2(b, a) * P.cK[i]);
+    }
+    if (!finite) qq[0] = __builtin_nanf("");
+    scale = finite ? (float)(1.0 / inv) : 0.0f;
+  }
+}
+
 // Wrapped Lambda-scale query x and the closest point c of Lambda (either coset);
 // false for a non-finite query (x = 0 then).
-__device__ __forceinline__ bool closest_point(const float* __restrict__ q, bool have, const Params P, float (&x)[8],
+__device__ __forceinline__ bool closest_point(const float (&qq)[8], bool have, const Params P, float (&x)[8],
                                               int (&c)[8]) {
   bool valid = have;
   if (have) {
-    float4 a = reinterpret_cast<const float4*>(q)[0];
-    float4 b = reinterpret_cast<const float4*>(q)[1];
-    float qq[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       float xi = 2.0f * qq[i];
@@ -205,10 +239,14 @@ __device__ __forceinline__ bool closest_point(const float* __restrict__ q, bool 
   return valid;
 }
 
-__device__ __forceinline__ void make_frame(const float* __restrict__ q, bool have, const Params P, Frame& F) {
+template <bool TH>
+__device__ __forceinline__ void make_frame(const float* __restrict__ in, bool have, const Params P, Frame& F) {
   float x[8];
   int c[8];
-  const bool valid = closest_point(q, have, P, x, c);
+  float qq[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  float scale = 0.0f;
+  if (have) load_query<TH>(in, P, qq, scale);
+  const bool valid = closest_point(qq, have, P, x, c);
   float a[8];
   uint32_t neg = 0;
 #pragma unroll
@@ -244,7 +282,7 @@ __device__ __forceinline__ void make_frame(const float* __restrict__ q, bool hav
   w.z = (uint32_t)(uint16_t)c[4] | ((uint32_t)(uint16_t)c[5] << 16);
   w.w = (uint32_t)(uint16_t)c[6] | ((uint32_t)(uint16_t)c[7] << 16);
   reinterpret_cast<uint4*>(F.c)[0] = w;
-  reinterpret_cast<uint4*>(&F.misc)[0] = make_uint4(neg | (valid ? 0x100u : 0u), 0u, 0u, 0u);
+  reinterpret_cast<uint4*>(&F.misc)[0] = make_uint4(neg | (valid ? 0x100u : 0u), __float_as_uint(scale), 0u, 0u);
 }
 
 // ---------------------------------------------------------------------------
@@ -608,7 +646,7 @@ struct Search {
         n.slot = cand_slot(S.st, n.lo, n.hi, sel);
         const float u = 1.0f - __uint_as_float(n.dbits) * 0.125f;
         const float u2 = u * u;
-        W.wgt[buf][lane] = u2 * u2;
+        W.wgt[buf][lane] = (u2 * u2) * F.s;  // exact for plain lookups (s = 1)
       } else {
         n.lo = n.hi = 0;
         n.dbits = KEY_INF;
@@ -621,21 +659,27 @@ struct Search {
   }
 };
 
+// Input floats per lookup: q (8) or z (16, the activation layer).
+template <bool TH>
+constexpr int in_stride() { return TH ? 16 : 8; }
+
 // Phase A for the wave's lookups [base, base + lpw).
-__device__ __forceinline__ void phase_a(const float* __restrict__ q, int64_t base, int nl, const Params P,
+template <bool TH>
+__device__ __forceinline__ void phase_a(const float* __restrict__ in, int64_t base, int nl, const Params P,
                                         Frame* frames, int lane) {
-  if (lane < nl) make_frame(q + (base + lane) * 8, true, P, frames[lane]);
+  if (lane < nl) make_frame<TH>(in + (base + lane) * in_stride<TH>(), true, P, frames[lane]);
   wave_lds_sync();
 }
 
 // Same, for the lookups perm[base .. base + nl) of a reordered batch; returns
 // this lane's lookup index (lane t holds the lookup of position base + t).
-__device__ __forceinline__ uint32_t phase_a_perm(const float* __restrict__ q, const uint2* __restrict__ perm,
+template <bool TH>
+__device__ __forceinline__ uint32_t phase_a_perm(const float* __restrict__ in, const uint2* __restrict__ perm,
                                                  int64_t base, int nl, const Params P, Frame* frames, int lane) {
   uint32_t l = 0;
   if (lane < nl) {
     l = perm[base + lane].x;
-    make_frame(q + (size_t)l * 8, true, P, frames[lane]);
+    make_frame<TH>(in + (size_t)l * in_stride<TH>(), true, P, frames[lane]);
   }
   wave_lds_sync();
   return l;
@@ -668,7 +712,7 @@ __global__ void __launch_bounds__(THREADS) k_neighbors(const float* __restrict__
   Search srch(P, S.tab, S.wave[c.wave], c.wave, c.lane);
   WaveLds& W = S.wave[c.wave];
   Frame* FR = S.frames[c.wave];
-  phase_a(q, c.base, c.nl, P, FR, c.lane);
+  phase_a<false>(q, c.base, c.nl, P, FR, c.lane);
   for (int t = 0; t < c.nl; ++t) {
     const Frame& F = FR[t];
     const Sel sel = read_sel(F);
@@ -798,7 +842,9 @@ __device__ __forceinline__ void fwd_consume(const WaveLds& W, int buf, int lane,
   }
 }
 
-template <int DT, int M>
+// TH: the input is the activation layer's z [L][16] instead of q [L][8]; the
+// scale s is folded into the weights by the search.
+template <int DT, int M, bool TH>
 __global__ void __launch_bounds__(THREADS) k_forward(const float* __restrict__ q, Params P,
                                                      const void* __restrict__ table, void* __restrict__ out) {
   using G = FwdGeom<DT, M>;
@@ -808,7 +854,7 @@ __global__ void __launch_bounds__(THREADS) k_forward(const float* __restrict__ q
   Search srch(P, S.tab, S.wave[c.wave], c.wave, c.lane);
   WaveLds& W = S.wave[c.wave];
   Frame* FR = S.frames[c.wave];
-  phase_a(q, c.base, c.nl, P, FR, c.lane);
+  phase_a<TH>(q, c.base, c.nl, P, FR, c.lane);
   const char* tb = reinterpret_cast<const char*>(table);
   uint32_t v[G::NI][G::DW];
   srch.run(FR[0], read_sel(FR[0]), 0);
@@ -842,15 +888,23 @@ __device__ __forceinline__ void scatter_atomic(const WaveLds& W, const float* __
 }
 
 // dq_i = sum_j -2 u_j^3 (x_i - k_{j,i}) <G, v_j> of one lookup (zero without
-// neighbours), written to gq[l].
-template <int DT, int M>
+// neighbours), written to gq[l][8].
+// TH (activation layer): also dL/ds = sum_j w_j <G, v_j> = <G, phi>, and the
+// chain through q_i = c_i arg z_i and s = (sum 1/|z_i|)^-1 (Sec. 2.3), with
+// dL/dq = s dq:
+//   dL/da_i = dL/ds s^2 a_i / r_i^3 - dL/dq_i c_i b_i / r_i^2,
+//   dL/db_i = dL/ds s^2 b_i / r_i^3 + dL/dq_i c_i a_i / r_i^2,
+// written to gq[l][16] (zero where s = 0); zin is z.
+template <int DT, int M, bool TH>
 __device__ __forceinline__ void grad_query(const Frame& F, const WaveLds& W, const Tables& T, int count,
                                            const char* __restrict__ tb, const float* __restrict__ gout, int64_t l,
-                                           int lane, float* __restrict__ gq) {
+                                           int lane, float* __restrict__ gq, const float* __restrict__ zin,
+                                           const Params& P) {
   using G = RowGeom<DT, M>;
   constexpr int ICOORD = G::LPR >= 8 ? 1 : 8 / G::LPR;  // query coordinates per lane
   const int rsub = lane / G::LPR, ch = lane % G::LPR;
   float dq[ICOORD];
+  double dls = 0.0;  // dL/ds (TH)
 #pragma unroll
   for (int k = 0; k < ICOORD; ++k) dq[k] = 0.0f;
   if (count > 0) {
@@ -880,16 +934,34 @@ __device__ __forceinline__ void grad_query(const Frame& F, const WaveLds& W, con
       const int j = p * G::RPP + rsub;
       float f[G::EPC];
       unpack16<DT, G::EPC>(v[p], f);
-      float pd = 0.0f;
+      // <G, v_j>: this lane's chunk, then a sum over the LPR lanes of the row.
+      // Behind the activation layer it is formed in fp64 (fp32 x fp32
+      // products are exact there): dL/ds = sum_j w_j <G, v_j> can cancel
+      // deeply (at a lattice point it is one dot product and dq = 0), and it
+      // then carries the whole gradient of the lookup.
+      float pd;
+      double pd64 = 0.0;
+      if constexpr (!TH) {
+        pd = 0.0f;
 #pragma unroll
-      for (int e = 0; e < G::EPC; ++e) pd = fmaf(g[e], f[e], pd);
-      // <G, v_j>: sum over the LPR lanes of this row
+        for (int e = 0; e < G::EPC; ++e) pd = fmaf(g[e], f[e], pd);
 #pragma unroll
-      for (int mask = 1; mask < G::LPR; mask <<= 1) pd += __shfl_xor(pd, mask);
+        for (int mask = 1; mask < G::LPR; mask <<= 1) pd += __shfl_xor(pd, mask);
+      } else {
+#pragma unroll
+        for (int e = 0; e < G::EPC; ++e) pd64 = fma((double)g[e], (double)f[e], pd64);
+#pragma unroll
+        for (int mask = 1; mask < G::LPR; mask <<= 1) pd64 += __shfl_xor(pd64, mask);
+        pd = (float)pd64;
+      }
       if (sl[p] >= 0) {
         const Nbr n = W.nbr[0][j];
         const float u = 1.0f - __uint_as_float(n.dbits) * 0.125f;
         const float a = -2.0f * u * u * u * pd;
+        if constexpr (TH) {
+          const float u2 = u * u;
+          dls = fma((double)(u2 * u2), pd64, dls);
+        }
 #pragma unroll
         for (int k = 0; k < ICOORD; ++k) {
           const int i = ch + k * G::LPR;
@@ -902,14 +974,35 @@ __device__ __forceinline__ void grad_query(const Frame& F, const WaveLds& W, con
     }
   }
 #pragma unroll
-  for (int mask = G::LPR; mask < WAVE; mask <<= 1)
+  for (int mask = G::LPR; mask < WAVE; mask <<= 1) {
 #pragma unroll
     for (int k = 0; k < ICOORD; ++k) dq[k] += __shfl_xor(dq[k], mask);
+    if constexpr (TH) dls += __shfl_xor(dls, mask);
+  }
   if (rsub == 0) {
 #pragma unroll
     for (int k = 0; k < ICOORD; ++k) {
       const int i = ch + k * G::LPR;
-      if (i < 8) gq[l * 8 + i] = dq[k];
+      if (i >= 8) continue;
+      if constexpr (!TH) {
+        gq[l * 8 + i] = dq[k];
+      } else {
+        double ci = P.cK[0];
+#pragma unroll
+        for (int e = 1; e < 8; ++e) ci = i == e ? P.cK[e] : ci;
+        const double sc = F.s;
+        double ga = 0.0, gb = 0.0;
+        if (sc > 0.0) {
+          const float2 ab = *reinterpret_cast<const float2*>(zin + l * 16 + 2 * i);
+          const double a = ab.x, b = ab.y;
+          const double r2 = a * a + b * b;
+          const double r3 = r2 * sqrt(r2);
+          const double ds = dls * sc * sc, dqs = (double)dq[k] * sc * ci;
+          ga = ds * a / r3 - dqs * b / r2;
+          gb = ds * b / r3 + dqs * a / r2;
+        }
+        *reinterpret_cast<float2*>(gq + l * 16 + 2 * i) = make_float2((float)ga, (float)gb);
+      }
     }
   }
 }
@@ -918,7 +1011,7 @@ __device__ __forceinline__ void grad_query(const Frame& F, const WaveLds& W, con
 // atomics (EMIT = false), or emitted as (location, (lookup, w_j)) pairs for
 // the sorted segmented reduction (EMIT = true; padding gets the key N, which
 // sorts last).
-template <int DT, int M, bool EMIT>
+template <int DT, int M, bool EMIT, bool TH>
 __global__ void __launch_bounds__(THREADS) k_backward(const float* __restrict__ q, Params P,
                                                       const void* __restrict__ table,
                                                       const float* __restrict__ gout, float* __restrict__ gtab,
@@ -931,7 +1024,7 @@ __global__ void __launch_bounds__(THREADS) k_backward(const float* __restrict__ 
   Search srch(P, S.tab, S.wave[c.wave], c.wave, lane);
   WaveLds& W = S.wave[c.wave];
   Frame* FR = S.frames[c.wave];
-  phase_a(q, c.base, c.nl, P, FR, lane);
+  phase_a<TH>(q, c.base, c.nl, P, FR, lane);
   const char* tb = reinterpret_cast<const char*>(table);
   for (int t = 0; t < c.nl; ++t) {
     const Frame& F = FR[t];
@@ -939,7 +1032,7 @@ __global__ void __launch_bounds__(THREADS) k_backward(const float* __restrict__ 
     const int count = srch.run(F, sel, 0);
     const int64_t l = c.base + t;
     if (!EMIT && gtab && count > 0) scatter_atomic<M>(W, gout, l, gtab, lane);
-    if (gq) grad_query<DT, M>(F, W, S.tab, count, tb, gout, l, lane, gq);
+    if (gq) grad_query<DT, M, TH>(F, W, S.tab, count, tb, gout, l, lane, gq, q, P);
     if (EMIT && gtab && lane < NB) {
       const int32_t s = W.nbr[0][lane].slot;
       pair_key[l * NB + lane] = s >= 0 ? (uint32_t)s : P.N;
@@ -1212,13 +1305,15 @@ __global__ void __launch_bounds__(THREADS) k_segreduce(const uint32_t* __restric
 
 // key[l] = location of the closest point of Lambda to q_l (N for a non-finite
 // query), val[l] = (l, 0).
+template <bool TH>
 __global__ void __launch_bounds__(THREADS) k_cell_key(const float* __restrict__ q, Params P,
                                                       uint32_t* __restrict__ key, uint2* __restrict__ val) {
   const int64_t l = (int64_t)blockIdx.x * THREADS + threadIdx.x;
   if (l >= P.L) return;
-  float x[8];
+  float x[8], qq[8], scale;
   int c[8];
-  const bool valid = closest_point(q + l * 8, true, P, x, c);
+  load_query<TH>(q + l * in_stride<TH>(), P, qq, scale);
+  const bool valid = closest_point(qq, true, P, x, c);
   uint32_t loc = P.N;
   if (valid) {
     const int eps = c[0] & 1;
@@ -1233,6 +1328,18 @@ __global__ void __launch_bounds__(THREADS) k_cell_key(const float* __restrict__ 
   }
   key[l] = loc;
   val[l] = make_uint2((uint32_t)l, 0u);
+}
+
+// Activation layer coordinates: q[l] (8 fp32) and scale s[l] as the lookups see them.
+__global__ void __launch_bounds__(THREADS) k_theta_coords(const float* __restrict__ z, Params P,
+                                                          float* __restrict__ q, float* __restrict__ s) {
+  const int64_t l = (int64_t)blockIdx.x * THREADS + threadIdx.x;
+  if (l >= P.L) return;
+  float qq[8], scale;
+  load_query<true>(z + l * 16, P, qq, scale);
+  reinterpret_cast<float4*>(q + l * 8)[0] = make_float4(qq[0], qq[1], qq[2], qq[3]);
+  reinterpret_cast<float4*>(q + l * 8)[1] = make_float4(qq[4], qq[5], qq[6], qq[7]);
+  if (s) s[l] = scale;
 }
 
 constexpr int64_t AUTO_MERGE_MIN = 131072;      // LRAM_SCATTER_AUTO merges from this many lookups on
@@ -1283,7 +1390,7 @@ struct alignas(16) FusedLds {
 // A batch in which fewer than a tenth of the lookups share their closest
 // point with a neighbour in the order (queries spread thinly over the torus)
 // has little to merge: it scatters with per-lookup atomics instead.
-template <int DT, int M>
+template <int DT, int M, bool TH>
 __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __restrict__ q, Params P,
                                                              const void* __restrict__ table,
                                                              const float* __restrict__ gout,
@@ -1307,7 +1414,7 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
       Search srch(P, S.b.search.tab, S.b.search.wave[wave], wave, lane);
       WaveLds& W = S.b.search.wave[wave];
       Frame* FR = S.b.search.frames[wave];
-      const uint32_t my_l = phase_a_perm(q, perm, base, nl, P, FR, lane);
+      const uint32_t my_l = phase_a_perm<TH>(q, perm, base, nl, P, FR, lane);
       const char* tb = reinterpret_cast<const char*>(table);
       for (int i = 0; i < nl; ++i) {
         const Frame& F = FR[i];
@@ -1315,7 +1422,7 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
         const int count = srch.run(F, sel, 0);
         const int64_t l = (int64_t)__builtin_amdgcn_readlane(my_l, i);
         if (!merge && count > 0) scatter_atomic<M>(W, gout, l, gtab, lane);
-        if (gq) grad_query<DT, M>(F, W, S.b.search.tab, count, tb, gout, l, lane, gq);
+        if (gq) grad_query<DT, M, TH>(F, W, S.b.search.tab, count, tb, gout, l, lane, gq, q, P);
         if (merge && lane < NB) {
           const int pidx = (wave * P.lpw + i) * NB + lane;
           S.a.pairs.loc[pidx] = W.nbr[0][lane].slot;
@@ -1464,6 +1571,7 @@ int check_common(const float* q, int64_t B, int64_t H, const int32_t* K, int64_t
     uint32_t s = 1;
     for (int j = i + 1; j < 8; ++j) s *= (uint32_t)K[j];
     P->S[i] = s;
+    P->cK[i] = (double)K[i] / (2.0 * 3.14159265358979323846);
   }
   P->N = (uint32_t)N;
   P->L = *L;
@@ -1508,8 +1616,11 @@ int dispatch(int dtype, int32_t m, Args... args) {
 
 template <int DT, int M>
 struct FwdLaunch {
-  static int go(const float* q, const Params& P, const void* table, void* out, hipStream_t s) {
-    hipLaunchKernelGGL((k_forward<DT, M>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, out);
+  static int go(const float* q, const Params& P, const void* table, void* out, bool th, hipStream_t s) {
+    if (th)
+      hipLaunchKernelGGL((k_forward<DT, M, true>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, out);
+    else
+      hipLaunchKernelGGL((k_forward<DT, M, false>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, out);
     return launched();
   }
 };
@@ -1607,12 +1718,17 @@ int radix_sort(const SortWs& ws, uint32_t N, hipStream_t s, uint32_t** kres, uin
   return LRAM_OK;
 }
 
+// q is the lookups' input: q [L][8], or z [L][16] when th (activation layer).
 template <int DT, int M>
 struct BwdAtomicLaunch {
-  static int go(const float* q, const Params& P, const void* table, const float* g, float* gt, float* gq,
+  static int go(const float* q, const Params& P, const void* table, const float* g, float* gt, float* gq, bool th,
                 hipStream_t s) {
-    hipLaunchKernelGGL((k_backward<DT, M, false>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g, gt,
-                       gq, (uint32_t*)nullptr, (uint2*)nullptr);
+    if (th)
+      hipLaunchKernelGGL((k_backward<DT, M, false, true>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g,
+                         gt, gq, (uint32_t*)nullptr, (uint2*)nullptr);
+    else
+      hipLaunchKernelGGL((k_backward<DT, M, false, false>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g,
+                         gt, gq, (uint32_t*)nullptr, (uint2*)nullptr);
     return launched();
   }
 };
@@ -1620,10 +1736,13 @@ struct BwdAtomicLaunch {
 template <int DT, int M>
 struct BwdMergedLaunch {
   static int go(const float* q, const Params& P, const void* table, const float* g, float* gt, float* gq,
-                const MergeWs& ws, hipStream_t s) {
-    if (!gt) return BwdAtomicLaunch<DT, M>::go(q, P, table, g, gt, gq, s);
-    hipLaunchKernelGGL(k_cell_key, dim3((unsigned)((P.L + THREADS - 1) / THREADS)), dim3(THREADS), 0, s, q, P,
-                       ws.sort.k0, ws.sort.v0);
+                const MergeWs& ws, bool th, hipStream_t s) {
+    if (!gt) return BwdAtomicLaunch<DT, M>::go(q, P, table, g, gt, gq, th, s);
+    const dim3 kgrid((unsigned)((P.L + THREADS - 1) / THREADS));
+    if (th)
+      hipLaunchKernelGGL(k_cell_key<true>, kgrid, dim3(THREADS), 0, s, q, P, ws.sort.k0, ws.sort.v0);
+    else
+      hipLaunchKernelGGL(k_cell_key<false>, kgrid, dim3(THREADS), 0, s, q, P, ws.sort.k0, ws.sort.v0);
     if (int rc = launched()) return rc;
     uint32_t* keys;
     uint2* perm;
@@ -1632,8 +1751,13 @@ struct BwdMergedLaunch {
     Params Pm = P;
     Pm.lpw = P.lpw < MERGE_LPW ? P.lpw : MERGE_LPW;
     const int64_t per_block = (int64_t)Pm.lpw * WAVES;
-    hipLaunchKernelGGL((k_backward_merged<DT, M>), dim3((unsigned)((P.L + per_block - 1) / per_block)),
-                       dim3(THREADS), 0, s, q, Pm, table, g, gt, gq, (const uint32_t*)keys, (const uint2*)perm);
+    const dim3 grid((unsigned)((P.L + per_block - 1) / per_block));
+    if (th)
+      hipLaunchKernelGGL((k_backward_merged<DT, M, true>), grid, dim3(THREADS), 0, s, q, Pm, table, g, gt, gq,
+                         (const uint32_t*)keys, (const uint2*)perm);
+    else
+      hipLaunchKernelGGL((k_backward_merged<DT, M, false>), grid, dim3(THREADS), 0, s, q, Pm, table, g, gt, gq,
+                         (const uint32_t*)keys, (const uint2*)perm);
     return launched();
   }
 };
@@ -1641,9 +1765,13 @@ struct BwdMergedLaunch {
 template <int DT, int M>
 struct BwdSortedLaunch {
   static int go(const float* q, const Params& P, const void* table, const float* g, float* gt, float* gq,
-                const SortWs& ws, hipStream_t s) {
-    hipLaunchKernelGGL((k_backward<DT, M, true>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g, gt,
-                       gq, ws.k0, ws.v0);
+                const SortWs& ws, bool th, hipStream_t s) {
+    if (th)
+      hipLaunchKernelGGL((k_backward<DT, M, true, true>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g,
+                         gt, gq, ws.k0, ws.v0);
+    else
+      hipLaunchKernelGGL((k_backward<DT, M, true, false>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g,
+                         gt, gq, ws.k0, ws.v0);
     int rc = launched();
     if (rc || !gt) return rc;
     uint32_t* kin;
@@ -1660,6 +1788,60 @@ struct BwdSortedLaunch {
     return launched();
   }
 };
+
+int forward_impl(const float* in, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype, int64_t N,
+                 int32_t m, void* out, bool th, hipStream_t stream) {
+  int64_t L;
+  Params P;
+  int rc = check_common(in, B, H, K, &L, &P);
+  if (rc) return rc;
+  rc = check_table(table, dtype, N, m, P, L);
+  if (rc) return rc;
+  if (L == 0) return LRAM_OK;
+  if (!out || (reinterpret_cast<uintptr_t>(out) & 15)) return LRAM_EINVAL;
+  return dispatch<FwdLaunch>(dtype, m, in, P, table, out, th, stream);
+}
+
+int resolve_mode(int64_t B, int64_t H, int mode, int* resolved);
+
+int backward_impl(const float* in, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
+                  int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_in, int mode,
+                  void* workspace, size_t ws_bytes, bool th, hipStream_t stream) {
+  int64_t L;
+  Params P;
+  int rc = check_common(in, B, H, K, &L, &P);
+  if (rc) return rc;
+  rc = check_table(table, dtype, N, m, P, L);
+  if (rc) return rc;
+  if ((rc = resolve_mode(B, H, mode, &mode))) return rc;
+  if (L == 0) return LRAM_OK;
+  if (!grad_out || (reinterpret_cast<uintptr_t>(grad_out) & 15)) return LRAM_EINVAL;
+  if (!grad_table && !grad_in) return LRAM_EINVAL;
+  if (grad_table && (reinterpret_cast<uintptr_t>(grad_table) & 15)) return LRAM_EINVAL;
+  if (grad_in && (reinterpret_cast<uintptr_t>(grad_in) & 15)) return LRAM_EINVAL;
+  if (mode == LRAM_SCATTER_ATOMIC)
+    return dispatch<BwdAtomicLaunch>(dtype, m, in, P, table, grad_out, grad_table, grad_in, th, stream);
+  if (L > INT64_MAX / NB || L * NB >= (int64_t(1) << 32)) return LRAM_EINVAL;  // positions are 32-bit
+  if (mode == LRAM_SCATTER_MERGED) {
+    const size_t need = merge_ws_layout(L, nullptr, nullptr);
+    if (!workspace || ws_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LRAM_EWORKSPACE;
+    MergeWs ws;
+    merge_ws_layout(L, &ws, reinterpret_cast<char*>(workspace));
+    return dispatch<BwdMergedLaunch>(dtype, m, in, P, table, grad_out, grad_table, grad_in, ws, th, stream);
+  }
+  const size_t need = sort_ws_layout(L, nullptr, nullptr);
+  if (!workspace || ws_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LRAM_EWORKSPACE;
+  SortWs ws;
+  sort_ws_layout(L, &ws, reinterpret_cast<char*>(workspace));
+  return dispatch<BwdSortedLaunch>(dtype, m, in, P, table, grad_out, grad_table, grad_in, ws, th, stream);
+}
+
+int resolve_mode(int64_t B, int64_t H, int mode, int* resolved) {
+  if (!resolved || B < 0 || H < 0 || (H != 0 && B > INT64_MAX / H)) return LRAM_EINVAL;
+  if (mode < LRAM_SCATTER_ATOMIC || mode > LRAM_SCATTER_AUTO) return LRAM_EMODE;
+  *resolved = mode != LRAM_SCATTER_AUTO ? mode : (B * H >= AUTO_MERGE_MIN ? LRAM_SCATTER_MERGED : LRAM_SCATTER_ATOMIC);
+  return LRAM_OK;
+}
 
 }  // namespace
 
@@ -1696,28 +1878,34 @@ int lram_neighbors(const float* q, int64_t B, int64_t H, const int32_t K[8], int
 
 int lram_forward(const float* q, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
                  int64_t N, int32_t m, void* out, void* stream) {
+  return forward_impl(q, B, H, K, table, dtype, N, m, out, false, (hipStream_t)stream);
+}
+
+int lram_theta_forward(const float* z, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
+                       int64_t N, int32_t m, void* out, void* stream) {
+  return forward_impl(z, B, H, K, table, dtype, N, m, out, true, (hipStream_t)stream);
+}
+
+int lram_theta_coords(const float* z, int64_t B, int64_t H, const int32_t K[8], float* q, float* s, void* stream) {
   int64_t L;
   Params P;
-  int rc = check_common(q, B, H, K, &L, &P);
-  if (rc) return rc;
-  rc = check_table(table, dtype, N, m, P, L);
+  int rc = check_common(z, B, H, K, &L, &P);
   if (rc) return rc;
   if (L == 0) return LRAM_OK;
-  if (!out || (reinterpret_cast<uintptr_t>(out) & 15)) return LRAM_EINVAL;
-  return dispatch<FwdLaunch>(dtype, m, q, P, table, out, (hipStream_t)stream);
+  if (!q || (reinterpret_cast<uintptr_t>(q) & 15)) return LRAM_EINVAL;
+  hipLaunchKernelGGL(k_theta_coords, dim3((unsigned)((L + THREADS - 1) / THREADS)), dim3(THREADS), 0,
+                     (hipStream_t)stream, z, P, q, s);
+  return launched();
 }
 
 int lram_scatter_mode_resolved(int64_t B, int64_t H, int mode, int* resolved) {
-  if (!resolved || B < 0 || H < 0 || (H != 0 && B > INT64_MAX / H)) return LRAM_EINVAL;
-  if (mode < LRAM_SCATTER_ATOMIC || mode > LRAM_SCATTER_AUTO) return LRAM_EMODE;
-  *resolved = mode != LRAM_SCATTER_AUTO ? mode : (B * H >= AUTO_MERGE_MIN ? LRAM_SCATTER_MERGED : LRAM_SCATTER_ATOMIC);
-  return LRAM_OK;
+  return resolve_mode(B, H, mode, resolved);
 }
 
 int lram_backward_workspace_bytes(int64_t B, int64_t H, int32_t m, int mode, size_t* bytes) {
   if (!bytes || B < 0 || H < 0) return LRAM_EINVAL;
   if (m != 32 && m != 64) return LRAM_EDTYPE;
-  if (int rc = lram_scatter_mode_resolved(B, H, mode, &mode)) return rc;
+  if (int rc = resolve_mode(B, H, mode, &mode)) return rc;
   if (mode == LRAM_SCATTER_ATOMIC) {
     *bytes = 0;
     return LRAM_OK;
@@ -1734,34 +1922,15 @@ int lram_backward_workspace_bytes(int64_t B, int64_t H, int32_t m, int mode, siz
 int lram_backward(const float* q, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
                   int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_q, int mode,
                   void* workspace, size_t ws_bytes, void* stream) {
-  (void)workspace;
-  (void)ws_bytes;
-  int64_t L;
-  Params P;
-  int rc = check_common(q, B, H, K, &L, &P);
-  if (rc) return rc;
-  rc = check_table(table, dtype, N, m, P, L);
-  if (rc) return rc;
-  if (int rc2 = lram_scatter_mode_resolved(B, H, mode, &mode)) return rc2;
-  if (L == 0) return LRAM_OK;
-  if (!grad_out || (reinterpret_cast<uintptr_t>(grad_out) & 15)) return LRAM_EINVAL;
-  if (!grad_table && !grad_q) return LRAM_EINVAL;
-  if (grad_table && (reinterpret_cast<uintptr_t>(grad_table) & 15)) return LRAM_EINVAL;
-  if (mode == LRAM_SCATTER_ATOMIC)
-    return dispatch<BwdAtomicLaunch>(dtype, m, q, P, table, grad_out, grad_table, grad_q, (hipStream_t)stream);
-  if (L > INT64_MAX / NB || L * NB >= (int64_t(1) << 32)) return LRAM_EINVAL;  // positions are 32-bit
-  if (mode == LRAM_SCATTER_MERGED) {
-    const size_t need = merge_ws_layout(L, nullptr, nullptr);
-    if (!workspace || ws_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LRAM_EWORKSPACE;
-    MergeWs ws;
-    merge_ws_layout(L, &ws, reinterpret_cast<char*>(workspace));
-    return dispatch<BwdMergedLaunch>(dtype, m, q, P, table, grad_out, grad_table, grad_q, ws, (hipStream_t)stream);
-  }
-  const size_t need = sort_ws_layout(L, nullptr, nullptr);
-  if (!workspace || ws_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LRAM_EWORKSPACE;
-  SortWs ws;
-  sort_ws_layout(L, &ws, reinterpret_cast<char*>(workspace));
-  return dispatch<BwdSortedLaunch>(dtype, m, q, P, table, grad_out, grad_table, grad_q, ws, (hipStream_t)stream);
+  return backward_impl(q, B, H, K, table, dtype, N, m, grad_out, grad_table, grad_q, mode, workspace, ws_bytes,
+                       false, (hipStream_t)stream);
+}
+
+int lram_theta_backward(const float* z, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
+                        int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_z, int mode,
+                        void* workspace, size_t ws_bytes, void* stream) {
+  return backward_impl(z, B, H, K, table, dtype, N, m, grad_out, grad_table, grad_z, mode, workspace, ws_bytes,
+                       true, (hipStream_t)stream);
 }
 
 }  // extern "C"

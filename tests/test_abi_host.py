@@ -97,6 +97,20 @@ def test_backward_validation(lib):
     assert lib.lram_backward_workspace_bytes(4, 1, 48, 0, ctypes.byref(n)) == 3
 
 
+def test_theta_validation(lib):
+    K7 = (ctypes.c_int32 * 8)(*([4] * 7 + [7]))
+    assert lib.lram_theta_forward(FAKE, 4, 1, K7, FAKE, 0, 4 ** 8, 32, FAKE, None) == 2
+    assert lib.lram_theta_forward(None, 4, 1, K4, FAKE, 0, 4 ** 8, 32, FAKE, None) == 1
+    assert lib.lram_theta_forward(FAKE_MIS, 4, 1, K4, FAKE, 0, 4 ** 8, 32, FAKE, None) == 1
+    assert lib.lram_theta_forward(FAKE, 4, 1, K4, FAKE, 0, 4 ** 8, 40, FAKE, None) == 3
+    assert lib.lram_theta_forward(None, 0, 3, K4, None, 0, 4 ** 8, 32, None, None) == 0
+    assert lib.lram_theta_coords(FAKE, 4, 1, K4, None, None, None) == 1
+    assert lib.lram_theta_coords(None, 0, 1, K4, None, None, None) == 0
+    assert lib.lram_theta_backward(FAKE, 4, 1, K4, FAKE, 0, 4 ** 8, 32, FAKE, None, None, 0, None, 0, None) == 1
+    assert lib.lram_theta_backward(FAKE, 4, 1, K4, FAKE, 0, 4 ** 8, 32, FAKE, FAKE, FAKE, 7, None, 0, None) == 5
+    assert lib.lram_theta_backward(FAKE, 4, 1, K4, FAKE, 0, 4 ** 8, 32, FAKE, FAKE, FAKE, 2, None, 0, None) == 4
+
+
 def test_auto_mode(lib):
     r = ctypes.c_int(-1)
     assert lib.lram_scatter_mode_resolved(4, 1, 3, ctypes.byref(r)) == 0 and r.value == 0        # small: atomic

@@ -116,6 +116,20 @@ def queries(w: Workload, seed: int = 0) -> np.ndarray:
     return _wrap(q, w.K).reshape(B, w.H, 8)
 
 
+def theta_inputs(w: Workload, seed: int = 0) -> np.ndarray:
+    """Inputs [B, H, 16] fp32 for the activation layer that land on the
+    workload's queries: z_i = r_i (cos t_i, sin t_i) with t_i = 2 pi q_i / K_i
+    (interleaved Re, Im) and moduli r_i ~ Rayleigh(1) (|N(0,1) + i N(0,1)| / sqrt 2,
+    the modulus of a random complex projection)."""
+    q = queries(w, seed).astype(np.float64)
+    r = np.random.Generator(np.random.PCG64(np.random.SeedSequence(seed + 7))).rayleigh(1.0, q.shape)
+    t = 2.0 * np.pi * q / np.asarray(w.K, np.float64)
+    z = np.empty(q.shape[:-1] + (16,), np.float32)
+    z[..., 0::2] = r * np.cos(t)
+    z[..., 1::2] = r * np.sin(t)
+    return z
+
+
 def make_table(w: Workload, device, seed: int = 0, chunk_rows: int = 1 << 22):
     """Value table [N, m] on ``device``: fp32 N(0, 0.02^2), cast with RNE for bf16."""
     import torch
