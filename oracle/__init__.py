@@ -68,6 +68,8 @@ def _load():
             P = ctypes.c_void_p
             lib.lram_oracle_neighbors.argtypes = [P, ctypes.c_int64, P, P, P, P, P, P, P, P, P, P]
             lib.lram_oracle_neighbors.restype = ctypes.c_int
+            lib.lram_oracle_neighbors_k.argtypes = [P, ctypes.c_int64, P, ctypes.c_int32, P, P, P, P, P, P, P, P, P]
+            lib.lram_oracle_neighbors_k.restype = ctypes.c_int
             lib.lram_oracle_locations.argtypes = [P, ctypes.c_int64, P, P]
             lib.lram_oracle_locations.restype = None
             lib.lram_oracle_recipe_d2.argtypes = [P, P, ctypes.c_int64, P]
@@ -89,9 +91,19 @@ def _check_k(K) -> np.ndarray:
     return K
 
 
-def neighbors(q: np.ndarray, K) -> dict:
-    """Closest-32 neighbour lists of queries q[..., 8] (user scale) on torus K."""
+ALL_WIDTH = 256  # list width of the untruncated lookup (the support holds at most 241 points)
+
+
+def neighbors(q: np.ndarray, K, k: int = 32) -> dict:
+    """Closest-k neighbour lists of queries q[..., 8] (user scale) on torus K.
+
+    k = 32 is the truncation of Sec. 2.6; other k keep the closest min(k, count)
+    points in the same order; k = 0 keeps the whole support (the untruncated
+    sum of Sec. 2.2 / 2.5) in lists of width ALL_WIDTH."""
     K = _check_k(K)
+    width = ALL_WIDTH if k == 0 else int(k)
+    if width < 1:
+        raise ValueError("k must be positive, or 0 for the whole support")
     q = np.ascontiguousarray(np.asarray(q, dtype=np.float32))
     lead = q.shape[:-1]
     assert q.shape[-1] == 8
@@ -99,17 +111,17 @@ def neighbors(q: np.ndarray, K) -> dict:
     L = qf.shape[0]
     x = np.empty((L, 8), np.float32)
     count = np.empty(L, np.int32)
-    slot = np.empty((L, NB), np.int32)
-    d2 = np.empty((L, NB), np.float32)
-    d64 = np.empty((L, NB), np.float64)
-    w64 = np.empty((L, NB), np.float64)
-    w32 = np.empty((L, NB), np.float32)
-    lift = np.empty((L, NB, 8), np.int32)
+    slot = np.empty((L, width), np.int32)
+    d2 = np.empty((L, width), np.float32)
+    d64 = np.empty((L, width), np.float64)
+    w64 = np.empty((L, width), np.float64)
+    w32 = np.empty((L, width), np.float32)
+    lift = np.empty((L, width, 8), np.int32)
     wsum = np.empty(L, np.float64)
     if L:
-        rc = _load().lram_oracle_neighbors(_ptr(qf), L, _ptr(K), _ptr(x), _ptr(count), _ptr(slot),
-                                           _ptr(d2), _ptr(d64), _ptr(w64), _ptr(w32), _ptr(lift),
-                                           _ptr(wsum))
+        rc = _load().lram_oracle_neighbors_k(_ptr(qf), L, _ptr(K), ctypes.c_int32(width), _ptr(x), _ptr(count),
+                                             _ptr(slot), _ptr(d2), _ptr(d64), _ptr(w64), _ptr(w32), _ptr(lift),
+                                             _ptr(wsum))
         if rc != 0:
             raise RuntimeError("oracle: support larger than expected")
     out = dict(x=x, count=count, slot=slot, d2=d2, d64=d64, w64=w64, w32=w32, lift=lift, wsum=wsum)
@@ -171,8 +183,9 @@ def grad_table_rows(nb: dict, G: np.ndarray):
     """Value-table gradient as (unique slots, rows): dV[s] = sum_{(l,j): slot=s} w_j G_l, fp64."""
     G = np.asarray(G, np.float64)
     m = G.shape[-1]
-    slot = nb["slot"].reshape(-1, NB)
-    w = nb["w64"].reshape(-1, NB)
+    width = nb["slot"].shape[-1]
+    slot = nb["slot"].reshape(-1, width)
+    w = nb["w64"].reshape(-1, width)
     Gf = G.reshape(-1, m)
     valid = slot >= 0
     s = slot[valid]

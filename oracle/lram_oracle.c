@@ -174,11 +174,14 @@ static double kernel64(double d2) {
  *   lift   [L][32][8] int32 the lattice points themselves (padding: 0)
  *   wsum   [L]      fp64  total kernel weight over the full support
  * Returns 0, or -1 if some query had more than ORACLE_MAXPTS support points
- * (impossible for E8: at most 121).
+ * (impossible for E8: at most 241 even on the closed ball).
+ * lram_oracle_neighbors_k writes `width` entries per lookup instead of 32:
+ * the closest min(width, count) points in the same order (width >= 241 keeps
+ * the whole support, i.e. the untruncated sum of Sec. 2.2 / 2.5).
  */
-int lram_oracle_neighbors(const float* q, int64_t L, const int32_t* K, float* x_out,
-                          int32_t* count, int32_t* slot, float* d2, double* d64,
-                          double* w64, float* w32, int32_t* lift, double* wsum) {
+int lram_oracle_neighbors_k(const float* q, int64_t L, const int32_t* K, int32_t width, float* x_out,
+                            int32_t* count, int32_t* slot, float* d2, double* d64,
+                            double* w64, float* w32, int32_t* lift, double* wsum) {
   int64_t N = 1;
   for (int i = 0; i < 8; i++) N *= K[i];
   int bad = 0;
@@ -205,8 +208,8 @@ int lram_oracle_neighbors(const float* q, int64_t L, const int32_t* K, float* x_
     double total = 0.0;
     for (int j = 0; j < c.n; j++) total += kernel64(recs[j].d64);
     wsum[l] = total;
-    for (int j = 0; j < ORACLE_NB; j++) {
-      int64_t o = l * ORACLE_NB + j;
+    for (int j = 0; j < width; j++) {
+      int64_t o = l * width + j;
       if (j < c.n) {
         const rec_t* r = &recs[j];
         slot[o] = r->slot;
@@ -228,6 +231,13 @@ int lram_oracle_neighbors(const float* q, int64_t L, const int32_t* K, float* x_
     }
   }
   return bad ? -1 : 0;
+}
+
+/* The closest-32 lists (Sec. 2.6). */
+int lram_oracle_neighbors(const float* q, int64_t L, const int32_t* K, float* x_out,
+                          int32_t* count, int32_t* slot, float* d2, double* d64,
+                          double* w64, float* w32, int32_t* lift, double* wsum) {
+  return lram_oracle_neighbors_k(q, L, K, ORACLE_NB, x_out, count, slot, d2, d64, w64, w32, lift, wsum);
 }
 
 /* Location of explicit lattice points (for tests of the bijection). */
