@@ -55,6 +55,8 @@ extern "C" {
 #endif
 
 #define LRAM_NEIGHBOURS 32
+#define LRAM_ALL 0            /* k of the untruncated lookup: every point of the support */
+#define LRAM_MAX_SUPPORT 256  /* list width of the untruncated lookup */
 
 typedef enum {
   LRAM_OK = 0,
@@ -137,6 +139,34 @@ int lram_scatter_mode_resolved(int64_t B, int64_t H, int mode, int* resolved);
 int lram_backward(const float* q, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
                   int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_q, int mode,
                   void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * Variable k and the untruncated lookup (Sec. 2.2 and 2.5: the sum over every
+ * lattice point in the support; Sec. 2.6: the truncation to the closest k,
+ * whose k = 32 is what every other entry point uses).  k is 16, 32, 64 or
+ * LRAM_ALL; otherwise LRAM_EINVAL.  The selection is the closest min(k, count)
+ * points in the order of the conventions above; LRAM_ALL keeps every point
+ * whose recipe distance is below 8.  That is at most 121 points in exact
+ * arithmetic (Table 1); the recipe's rounding can admit points at distance
+ * exactly sqrt 8, but never more than the 1 + 240 that a ball of that radius
+ * holds, so LRAM_ALL lists are LRAM_MAX_SUPPORT wide.  Lists are padded with
+ * slot -1, weight 0.  The backward scatters with fp32 atomics (the sorted and
+ * merged scatters take k = 32 only) and needs no workspace.
+ */
+
+/* lram_neighbors_k -- as lram_neighbors with lists of width w = k (LRAM_MAX_SUPPORT
+ * for LRAM_ALL): slot/w/d2 are [L][w]. */
+int lram_neighbors_k(const float* q, int64_t B, int64_t H, const int32_t K[8], int32_t k, int32_t* slot, float* w,
+                     float* d2, void* stream);
+
+/* lram_forward_k -- out[l] = sum over the closest min(k, count) points of w_j table[slot_j]. */
+int lram_forward_k(const float* q, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
+                   int64_t N, int32_t m, int32_t k, void* out, void* stream);
+
+/* lram_backward_k -- lram_backward's gradients for the k-point lookup (atomic scatter). */
+int lram_backward_k(const float* q, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
+                    int64_t N, int32_t m, int32_t k, const float* grad_out, float* grad_table, float* grad_q,
+                    void* stream);
 
 /*
  * Activation layer in front of the lookup (Sec. 2.3).  Each lookup takes 8

@@ -179,13 +179,18 @@ def grad_query(nb: dict, rows: np.ndarray, G: np.ndarray) -> np.ndarray:
     return np.einsum("...j,...ji->...i", a, e)
 
 
-def grad_table_rows(nb: dict, G: np.ndarray):
-    """Value-table gradient as (unique slots, rows): dV[s] = sum_{(l,j): slot=s} w_j G_l, fp64."""
+def grad_table_rows(nb: dict, G: np.ndarray, weights: str = "w64"):
+    """Value-table gradient as (unique slots, rows): dV[s] = sum_{(l,j): slot=s} w_j G_l, fp64.
+
+    ``weights`` picks the kernel weights: "w64" (fp64 distance, the default)
+    or "w32" (the fp32 recipe weights, for comparisons in which the weights of
+    neighbours at the edge of the support, u = 1 - r^2/8 near the fp32
+    resolution of r^2, must not dominate a row)."""
     G = np.asarray(G, np.float64)
     m = G.shape[-1]
     width = nb["slot"].shape[-1]
     slot = nb["slot"].reshape(-1, width)
-    w = nb["w64"].reshape(-1, width)
+    w = nb[weights].reshape(-1, width).astype(np.float64)
     Gf = G.reshape(-1, m)
     valid = slot >= 0
     s = slot[valid]

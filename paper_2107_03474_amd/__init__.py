@@ -22,7 +22,8 @@ import torch  # noqa: F401  -- loads the HIP runtime liblram.so must share
 __all__ = ["neighbors", "forward", "backward", "backward_workspace_bytes", "lookup", "LramLookup",
            "library_path", "load", "LramError", "F32", "BF16", "SCATTER_ATOMIC", "SCATTER_SORTED",
            "SCATTER_MERGED", "SCATTER_AUTO", "resolved_mode", "NB",
-           "theta_coords", "theta_forward", "theta_backward", "ThetaLookup", "theta"]
+           "theta_coords", "theta_forward", "theta_backward", "ThetaLookup", "theta", "ALL", "MAX_SUPPORT",
+           "list_width"]
 
 NB = 32
 F32, BF16 = 0, 1
@@ -67,6 +68,12 @@ def load():
             lib.lram_scatter_mode_resolved.restype = I
             lib.lram_backward.argtypes = [P, I64, I64, P, P, I, I64, I32, P, P, P, I, P, ctypes.c_size_t, P]
             lib.lram_backward.restype = I
+            lib.lram_neighbors_k.argtypes = [P, I64, I64, P, I32, P, P, P, P]
+            lib.lram_neighbors_k.restype = I
+            lib.lram_forward_k.argtypes = [P, I64, I64, P, P, I, I64, I32, I32, P, P]
+            lib.lram_forward_k.restype = I
+            lib.lram_backward_k.argtypes = [P, I64, I64, P, P, I, I64, I32, I32, P, P, P, P]
+            lib.lram_backward_k.restype = I
             lib.lram_theta_coords.argtypes = [P, I64, I64, P, P, P, P]
             lib.lram_theta_coords.restype = I
             lib.lram_theta_forward.argtypes = [P, I64, I64, P, P, I, I64, I32, P, P]
@@ -123,28 +130,43 @@ def _bh(q: torch.Tensor, last: int = 8, name: str = "q") -> Tuple[int, int]:
     return q.shape[0], q.shape[1]
 
 
-def neighbors(q: torch.Tensor, K: Sequence[int], want_d2: bool = True):
-    """Neighbour lists: (slot int32, w fp32, d2 fp32 or None), each [..., 32]."""
+ALL = 0             # k of the untruncated lookup (every point of the support)
+MAX_SUPPORT = 256   # list width of the untruncated lookup
+
+
+def list_width(k: int) -> int:
+    return MAX_SUPPORT if k == ALL else int(k)
+
+
+def neighbors(q: torch.Tensor, K: Sequence[int], want_d2: bool = True, k: int = NB):
+    """Neighbour lists: (slot int32, w fp32, d2 fp32 or None), each [..., width]
+    with width = k (16, 32, 64) or MAX_SUPPORT for k = ALL."""
     lib = load()
     B, H = _bh(q)
     lead = q.shape[:-1]
-    slot = torch.empty(lead + (NB,), dtype=torch.int32, device=q.device)
-    w = torch.empty(lead + (NB,), dtype=torch.float32, device=q.device)
-    d2 = torch.empty(lead + (NB,), dtype=torch.float32, device=q.device) if want_d2 else None
-    _check(lib.lram_neighbors(_dev(q, "q", torch.float32), B, H, _K(K), _dev(slot, "slot"), _dev(w, "w"),
-                              _dev(d2, "d2") if d2 is not None else None, _stream(q)))
+    wd = list_width(k)
+    slot = torch.empty(lead + (wd,), dtype=torch.int32, device=q.device)
+    w = torch.empty(lead + (wd,), dtype=torch.float32, device=q.device)
+    d2 = torch.empty(lead + (wd,), dtype=torch.float32, device=q.device) if want_d2 else None
+    _check(lib.lram_neighbors_k(_dev(q, "q", torch.float32), B, H, _K(K), int(k), _dev(slot, "slot"), _dev(w, "w"),
+                                _dev(d2, "d2") if d2 is not None else None, _stream(q)))
     return slot, w, d2
 
 
-def forward(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], out: Optional[torch.Tensor] = None):
-    """phi(q): [..., m] in the table dtype."""
+def forward(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], out: Optional[torch.Tensor] = None,
+            k: int = NB):
+    """phi(q) over the closest k points (k = ALL: the whole support): [..., m] in the table dtype."""
     lib = load()
     B, H = _bh(q)
     N, m = table.shape
     if out is None:
         out = torch.empty(q.shape[:-1] + (m,), dtype=table.dtype, device=q.device)
-    _check(lib.lram_forward(_dev(q, "q", torch.float32), B, H, _K(K), _dev(table, "table"), _table_dtype(table),
-                            N, m, _dev(out, "out", table.dtype), _stream(q)))
+    if k == NB:
+        _check(lib.lram_forward(_dev(q, "q", torch.float32), B, H, _K(K), _dev(table, "table"), _table_dtype(table),
+                                N, m, _dev(out, "out", table.dtype), _stream(q)))
+    else:
+        _check(lib.lram_forward_k(_dev(q, "q", torch.float32), B, H, _K(K), _dev(table, "table"),
+                                  _table_dtype(table), N, m, int(k), _dev(out, "out", table.dtype), _stream(q)))
     return out
 
 
@@ -165,10 +187,10 @@ def backward_workspace_bytes(B: int, H: int, m: int, mode="auto") -> int:
 
 def backward(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], grad_out: torch.Tensor,
              grad_table: Optional[torch.Tensor] = None, want_grad_q: bool = True, mode="auto",
-             workspace: Optional[torch.Tensor] = None, grad_q: Optional[torch.Tensor] = None):
+             workspace: Optional[torch.Tensor] = None, grad_q: Optional[torch.Tensor] = None, k: int = NB):
     """Gradients: grad_table [N, m] fp32 is ACCUMULATED into (allocated zeroed if None,
     pass False to skip), grad_q [..., 8] fp32 (None unless want_grad_q; written into
-    ``grad_q`` when given)."""
+    ``grad_q`` when given).  k != 32 (variable k / ALL) scatters with atomics."""
     lib = load()
     B, H = _bh(q)
     N, m = table.shape
@@ -177,6 +199,12 @@ def backward(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], grad_out: t
     gq = None
     if want_grad_q:
         gq = grad_q if grad_q is not None else torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    if k != NB:
+        gt_ptr = _dev(grad_table, "grad_table", torch.float32) if grad_table is not False else None
+        _check(lib.lram_backward_k(_dev(q, "q", torch.float32), B, H, _K(K), _dev(table, "table"),
+                                   _table_dtype(table), N, m, int(k), _dev(grad_out, "grad_out", torch.float32),
+                                   gt_ptr, _dev(gq, "grad_q") if gq is not None else None, _stream(q)))
+        return (grad_table if grad_table is not False else None), gq
     mode_i = _MODES[mode]
     ws_bytes = backward_workspace_bytes(B, H, m, mode_i)
     if ws_bytes and workspace is None:

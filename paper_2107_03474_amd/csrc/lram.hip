@@ -46,6 +46,12 @@ constexpr int KMAX = 8192;  // per-coordinate torus side bound: lattice coordina
 
 // ties at the 32nd distance involve points of the support (at most 121 of them)
 constexpr int TIE_MAX = 128;
+// List width of the untruncated lookup (every point of the support).  The
+// support is an open ball of radius sqrt 8; fp32 rounding of the distance
+// recipe can admit points at distance exactly sqrt 8, so the count can pass
+// the 121 of exact arithmetic, but a ball of that radius never holds more
+// than the 1 + 240 points around a lattice point.
+constexpr int KALL = 256;
 constexpr uint32_t KEY_INF = 0x7F800000u;      // +inf: never selected
 constexpr uint32_t KEY_8 = 0x41000000u;        // 8.0f: support boundary (open ball)
 constexpr uint32_t KEY_4 = 0x40800000u;        // 4.0f: fewer than 32 points are ever closer
@@ -81,9 +87,11 @@ struct alignas(16) Nbr {
   int32_t slot;       // location, -1 for padding
 };
 
+// Per-wave search state for lists of KS neighbours.
+template <int KS>
 struct alignas(16) WaveLds {
-  Nbr nbr[2][NB];     // double-buffered: lookup t+1 is searched while t is consumed
-  float wgt[2][NB];
+  Nbr nbr[2][KS];     // double-buffered: lookup t+1 is searched while t is consumed
+  float wgt[2][KS];
   uint32_t tie[TIE_MAX][2];
   uint32_t hist[64];  // distance histogram of the selection, 64 buckets on [4, 8)
 };
@@ -95,11 +103,11 @@ struct alignas(16) Tables {
   float et[8 * 64];
 };
 
-// LDS of the search for FR lookups per wave.
-template <int FR>
+// LDS of the search for FR lookups per wave and lists of KS neighbours.
+template <int FR, int KS = NB>
 struct alignas(16) SearchLds {
   Tables tab;
-  WaveLds wave[WAVES];
+  WaveLds<KS> wave[WAVES];
   Frame frames[WAVES][FR];
 };
 
@@ -362,46 +370,46 @@ __device__ __forceinline__ int count_below(const uint32_t (&key)[NS], uint32_t t
   return c;
 }
 
-// Threshold selection of the closest 32 (Sec. 2.6) over NS candidate slots per
-// lane.  Returns the number selected; a slot is selected iff key < thr, or
+// Threshold selection of the closest ks (Sec. 2.6: ks = 32) over NS candidate
+// slots per lane.  Returns the number selected; a slot is selected iff key < thr, or
 // key == tie_key and it is among the `need` first of those in (location,
 // lattice point) order (tie_key = KEY_INF when there is no tie).  *suspect is
-// set when a point of the boundary list could enter the selection (the 32nd
-// distance is within 1e-3 of the support edge, or fewer than 32 points are in
+// set when a point of the boundary list could enter the selection (the ks-th
+// distance is within 1e-3 of the support edge, or fewer than ks points are in
 // the support).
 template <int NS>
-__device__ __forceinline__ int threshold32(const uint32_t (&key)[NS], uint32_t& thr, uint32_t& tie_key, int& need,
-                                           bool& suspect) {
+__device__ __forceinline__ int threshold_k(const uint32_t (&key)[NS], const int ks, uint32_t& thr, uint32_t& tie_key,
+                                           int& need, bool& suspect) {
   tie_key = KEY_INF;
   need = 0;
   const int n8 = count_below(key, KEY_8);
-  if (n8 <= NB) {
+  if (n8 <= ks) {
     thr = KEY_8;
     suspect = true;
     return n8;
   }
   // bisection on the (monotone) bit patterns of non-negative floats:
-  // invariant count(< lo) < 32 < count(< hi)
+  // invariant count(< lo) < ks < count(< hi)
   uint32_t lo_k = KEY_4, hi_k = KEY_8;
   int c = count_below(key, lo_k);
-  if (c == NB) {
+  if (c == ks) {
     thr = lo_k;
     suspect = false;
-    return NB;
+    return ks;
   }
-  if (c > NB) {
+  if (c > ks) {
     hi_k = lo_k;
     lo_k = 0;
   }
   while (hi_k - lo_k > 1) {
     const uint32_t mid = lo_k + ((hi_k - lo_k) >> 1);
     c = count_below(key, mid);
-    if (c == NB) {
+    if (c == ks) {
       thr = mid;
       suspect = mid > KEY_SUSPECT;
-      return NB;
+      return ks;
     }
-    if (c < NB)
+    if (c < ks)
       lo_k = mid;
     else
       hi_k = mid;
@@ -409,9 +417,9 @@ __device__ __forceinline__ int threshold32(const uint32_t (&key)[NS], uint32_t& 
   // several candidates share the distance bits lo_k at the 32nd place
   thr = lo_k;
   tie_key = lo_k;
-  need = NB - count_below(key, lo_k);
+  need = ks - count_below(key, lo_k);
   suspect = lo_k > KEY_SUSPECT;
-  return NB;
+  return ks;
 }
 
 // Inclusive prefix sum across the 64 lanes of a wave (DPP row shifts, then row
@@ -426,16 +434,16 @@ __device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x) {
   return x;
 }
 
-// Threshold selection of the closest 32 through a 64-bucket histogram of the
+// Threshold selection of the closest ks through a 64-bucket histogram of the
 // distance bits on [4, 8) (bucket = top six mantissa bits): one LDS atomic per
-// candidate, a wave prefix sum and one ballot locate the bucket of the 32nd
+// candidate, a wave prefix sum and one ballot locate the bucket of the ks-th
 // point; the bisection then only runs inside that bucket.  Same contract as
-// threshold32.
+// threshold_k.
 template <int NS>
-__device__ __forceinline__ int threshold32_hist(const uint32_t (&key)[NS], uint32_t* hist, int lane, uint32_t& thr,
-                                                uint32_t& tie_key, int& need, bool& suspect) {
+__device__ __forceinline__ int threshold_k_hist(const uint32_t (&key)[NS], uint32_t* hist, int lane, const int ks,
+                                                uint32_t& thr, uint32_t& tie_key, int& need, bool& suspect) {
   const int clow = count_below(key, KEY_4);
-  if (clow >= NB) return threshold32<NS>(key, thr, tie_key, need, suspect);  // never expected
+  if (clow >= ks) return threshold_k<NS>(key, ks, thr, tie_key, need, suspect);  // never expected
   hist[lane] = 0;
   wave_lds_sync();
 #pragma unroll
@@ -447,45 +455,46 @@ __device__ __forceinline__ int threshold32_hist(const uint32_t (&key)[NS], uint3
   const int n8 = clow + (int)__builtin_amdgcn_readlane(pre, 63);
   tie_key = KEY_INF;
   need = 0;
-  if (n8 <= NB) {
+  if (n8 <= ks) {
     thr = KEY_8;
     suspect = true;
     return n8;
   }
-  const uint64_t m = __ballot(clow + (int)pre >= NB);
+  const uint64_t m = __ballot(clow + (int)pre >= ks);
   const int b = (int)__builtin_ctzll(m);
   const int below = clow + (int)__builtin_amdgcn_readlane(pre, b) - (int)__builtin_amdgcn_readlane(h, b);
   const int inb = (int)__builtin_amdgcn_readlane(h, b);
   uint32_t lo_k = KEY_4 + ((uint32_t)b << 17), hi_k = lo_k + (1u << 17);
-  if (below + inb == NB) {
+  if (below + inb == ks) {
     thr = hi_k;
     suspect = hi_k > KEY_SUSPECT;
-    return NB;
+    return ks;
   }
-  // invariant count(< lo) = below < 32 < count(< hi)
+  // invariant count(< lo) = below < ks < count(< hi)
   while (hi_k - lo_k > 1) {
     const uint32_t mid = lo_k + ((hi_k - lo_k) >> 1);
     const int c = count_below(key, mid);
-    if (c == NB) {
+    if (c == ks) {
       thr = mid;
       suspect = mid > KEY_SUSPECT;
-      return NB;
+      return ks;
     }
-    if (c < NB)
+    if (c < ks)
       lo_k = mid;
     else
       hi_k = mid;
   }
   thr = lo_k;
   tie_key = lo_k;
-  need = NB - count_below(key, lo_k);
+  need = ks - count_below(key, lo_k);
   suspect = lo_k > KEY_SUSPECT;
-  return NB;
+  return ks;
 }
 
+template <int KS>
 struct Search {
   Tables& S;
-  WaveLds& W;
+  WaveLds<KS>& W;
   int lane;
   uint32_t wbyte;
   uint32_t lo[NS_STRICT], hi[NS_STRICT];
@@ -496,7 +505,7 @@ struct Search {
 
   // (the kernel argument is read field by field: holding a reference to it
   // would force the argument block into private memory)
-  __device__ Search(const Params P, Tables& s, WaveLds& wv, int w, int l)
+  __device__ Search(const Params P, Tables& s, WaveLds<KS>& wv, int w, int l)
       : S(s), W(wv), lane(l), wbyte(64u * (uint32_t)w) {
 #pragma unroll
     for (int k = 0; k < NS_STRICT; ++k) load_candidate<0>(lane + WAVE * k, wbyte, lo[k], hi[k]);
@@ -548,7 +557,7 @@ struct Search {
   }
 
   // Writes the selected candidates into W.nbr[buf][0..count) (slot-major, then
-  // lane order); ties at the 32nd place are broken by (location, lattice point).
+  // lane order); ties at the ks-th place are broken by (location, lattice point).
   template <int NS>
   __device__ __forceinline__ void emit(const uint32_t (&key)[NS], uint32_t thr, uint32_t tie_key, int need,
                                        const Sel& sel, const Frame& F, int buf) {
@@ -592,10 +601,11 @@ struct Search {
         p = rank < need;
       }
       const uint64_t m = __ballot(p);
-      if (p) {
+      const int pos = base + prefix_count(m);
+      if (p && pos < KS) {
         uint32_t l, h;
         cand(s, l, h);
-        Nbr& n = W.nbr[buf][base + prefix_count(m)];
+        Nbr& n = W.nbr[buf][pos];
         n.lo = l;
         n.hi = h;
         n.dbits = key[s];
@@ -604,7 +614,7 @@ struct Search {
     }
   }
 
-  // Full neighbour search of frame F into buffer `buf`: W.nbr[buf][0..32) with
+  // Full neighbour search of frame F into buffer `buf`: W.nbr[buf][0..KS) with
   // (lo, hi, dbits, slot) and W.wgt[buf] with the fp32 recipe weights, padded
   // with slot -1 / weight 0.  Returns the number of real neighbours.
   __device__ int run(const Frame& F, const Sel& sel, int buf) {
@@ -618,8 +628,8 @@ struct Search {
         key[k] = (lane + WAVE * k < E8_NSTRICT) ? __float_as_uint(cand_d2(S.qt, lo[k], hi[k], sel)) : KEY_INF;
       uint32_t thr, tie_key;
       int need;
-      bool suspect;
-      count = threshold32_hist<NS_STRICT>(key, W.hist, lane, thr, tie_key, need, suspect);
+      bool suspect = true;
+      if constexpr (KS != KALL) count = threshold_k_hist<NS_STRICT>(key, W.hist, lane, KS, thr, tie_key, need, suspect);
       if (!suspect) {
         emit<NS_STRICT>(key, thr, tie_key, need, sel, F, buf);
       } else {
@@ -633,25 +643,35 @@ struct Search {
           const bool okb = load_candidate<1>(lane + WAVE * k, wbyte, l, h);
           key7[NS_STRICT + k] = okb ? __float_as_uint(cand_d2(S.qt, l, h, sel)) : KEY_INF;
         }
-        bool suspect7;
-        count = threshold32<NS_ALL>(key7, thr, tie_key, need, suspect7);
-        emit<NS_ALL>(key7, thr, tie_key, need, sel, F, buf);
+        if constexpr (KS == KALL) {
+          // untruncated: every candidate whose recipe distance is below 8
+          count = min(count_below(key7, KEY_8), KS);
+          emit<NS_ALL>(key7, KEY_8, KEY_INF, 0, sel, F, buf);
+        } else {
+          bool suspect7;
+          count = threshold_k<NS_ALL>(key7, KS, thr, tie_key, need, suspect7);
+          emit<NS_ALL>(key7, thr, tie_key, need, sel, F, buf);
+        }
       }
       wave_lds_sync();
     }
     // locations and weights, one neighbour per lane
-    if (lane < NB) {
-      Nbr& n = W.nbr[buf][lane];
-      if (lane < count) {
-        n.slot = cand_slot(S.st, n.lo, n.hi, sel);
-        const float u = 1.0f - __uint_as_float(n.dbits) * 0.125f;
-        const float u2 = u * u;
-        W.wgt[buf][lane] = (u2 * u2) * F.s;  // exact for plain lookups (s = 1)
-      } else {
-        n.lo = n.hi = 0;
-        n.dbits = KEY_INF;
-        n.slot = -1;
-        W.wgt[buf][lane] = 0.0f;
+#pragma unroll
+    for (int r = 0; r < (KS + WAVE - 1) / WAVE; ++r) {
+      const int e = lane + WAVE * r;
+      if (e < KS) {
+        Nbr& n = W.nbr[buf][e];
+        if (e < count) {
+          n.slot = cand_slot(S.st, n.lo, n.hi, sel);
+          const float u = 1.0f - __uint_as_float(n.dbits) * 0.125f;
+          const float u2 = u * u;
+          W.wgt[buf][e] = (u2 * u2) * F.s;  // exact for plain lookups (s = 1)
+        } else {
+          n.lo = n.hi = 0;
+          n.dbits = KEY_INF;
+          n.slot = -1;
+          W.wgt[buf][e] = 0.0f;
+        }
       }
     }
     wave_lds_sync();
@@ -703,14 +723,16 @@ __device__ __forceinline__ bool wave_ctx(const Params P, WaveCtx& c) {
   return true;
 }
 
+// Neighbour lists of width KS (NB = 32: Sec. 2.6; KALL: the whole support).
+template <int KS>
 __global__ void __launch_bounds__(THREADS) k_neighbors(const float* __restrict__ q, Params P,
                                                        int32_t* __restrict__ slot_out, float* __restrict__ w_out,
                                                        float* __restrict__ d2_out) {
-  __shared__ SearchLds<WAVE> S;
+  __shared__ SearchLds<WAVE, KS> S;
   WaveCtx c;
   if (!wave_ctx(P, c)) return;
-  Search srch(P, S.tab, S.wave[c.wave], c.wave, c.lane);
-  WaveLds& W = S.wave[c.wave];
+  Search<KS> srch(P, S.tab, S.wave[c.wave], c.wave, c.lane);
+  WaveLds<KS>& W = S.wave[c.wave];
   Frame* FR = S.frames[c.wave];
   phase_a<false>(q, c.base, c.nl, P, FR, c.lane);
   for (int t = 0; t < c.nl; ++t) {
@@ -718,38 +740,43 @@ __global__ void __launch_bounds__(THREADS) k_neighbors(const float* __restrict__
     const Sel sel = read_sel(F);
     const int count = srch.run(F, sel, 0);
     const int64_t l = c.base + t;
-    if (c.lane < NB) {
+    for (int me_i = c.lane; me_i < KS; me_i += WAVE) {
       // order the list by (distance bits, location, lattice point)
-      const Nbr me = W.nbr[0][c.lane];
-      int rank = c.lane;
-      if (c.lane < count) {
+      const Nbr me = W.nbr[0][me_i];
+      int rank = me_i;
+      if (me_i < count) {
         const uint32_t mk = cand_liftkey(me.lo, me.hi, sel, F);
         rank = 0;
         for (int e = 0; e < count; ++e) {
           const Nbr o = W.nbr[0][e];
           bool less = o.dbits < me.dbits || (o.dbits == me.dbits && o.slot < me.slot);
-          if (o.dbits == me.dbits && o.slot == me.slot && e != c.lane) less = cand_liftkey(o.lo, o.hi, sel, F) < mk;
+          if (o.dbits == me.dbits && o.slot == me.slot && e != me_i) less = cand_liftkey(o.lo, o.hi, sel, F) < mk;
           rank += less ? 1 : 0;
         }
       }
-      slot_out[l * NB + rank] = me.slot;
-      w_out[l * NB + rank] = W.wgt[0][c.lane];
-      if (d2_out) d2_out[l * NB + rank] = __uint_as_float(me.dbits);
+      slot_out[l * KS + rank] = me.slot;
+      w_out[l * KS + rank] = W.wgt[0][me_i];
+      if (d2_out) d2_out[l * KS + rank] = __uint_as_float(me.dbits);
     }
     wave_lds_sync();
   }
 }
 
-template <int DT, int M>
+// Row geometry of the backward's table reads for chunks of R rows.
+template <int DT, int M, int R = NB>
 struct RowGeom {
   static constexpr int ES = DT == LRAM_F32 ? 4 : 2;      // table element bytes
   static constexpr int RB = M * ES;                       // row bytes
   static constexpr int LPR = RB / 16;                     // lanes per row (16 B each)
   static constexpr int RPP = WAVE / LPR;                  // rows per pass
-  static constexpr int NP = NB / RPP;                     // passes
+  static constexpr int NP = R / RPP;                      // passes
   static constexpr int EPC = 16 / ES;                     // elements per 16-byte chunk
-  static_assert(RB % 16 == 0 && LPR <= WAVE && NB % RPP == 0, "row geometry");
+  static_assert(RB % 16 == 0 && LPR <= WAVE && R % RPP == 0, "row geometry");
 };
+
+// Rows handled together by the gathers of a list of KS neighbours.
+template <int KS>
+constexpr int chunk_rows() { return KS < NB ? KS : NB; }
 
 template <int DT, int EPC>
 __device__ __forceinline__ void unpack16(const uint4 v, float (&f)[EPC]) {
@@ -770,27 +797,28 @@ __device__ __forceinline__ void unpack16(const uint4 v, float (&f)[EPC]) {
 // LPR lanes cover a row, one load instruction covers RPI rows, NI instructions
 // cover the 32 rows; a lane accumulates EPL output elements over its NI rows and
 // the RPI row groups are summed with xor shuffles.
-template <int DT, int M>
+template <int DT, int M, int R = NB>
 struct FwdGeom {
   static constexpr int ES = DT == LRAM_F32 ? 4 : 2;
   static constexpr int RB = M * ES;
   static constexpr int BPL = (DT == LRAM_F32 && M == 64) ? 8 : 4;
   static constexpr int LPR = RB / BPL;
   static constexpr int RPI = WAVE / LPR;
-  static constexpr int NI = NB / RPI;
+  static constexpr int NI = R / RPI;
   static constexpr int EPL = BPL / ES;
   static constexpr int DW = BPL / 4;  // dwords per lane per row
-  static_assert(LPR <= WAVE && WAVE % LPR == 0 && NB % RPI == 0, "forward gather geometry");
+  static_assert(LPR <= WAVE && WAVE % LPR == 0 && R % RPI == 0, "forward gather geometry");
 };
 
-template <int DT, int M>
-__device__ __forceinline__ void fwd_issue(const char* __restrict__ tb, const WaveLds& W, int buf, int lane,
-                                          uint32_t (&v)[FwdGeom<DT, M>::NI][FwdGeom<DT, M>::DW]) {
-  using G = FwdGeom<DT, M>;
+// Loads the rows r0 .. r0 + R of list `buf` (R = the geometry's chunk).
+template <int DT, int M, int KS, int R = NB>
+__device__ __forceinline__ void fwd_issue(const char* __restrict__ tb, const WaveLds<KS>& W, int buf, int lane,
+                                          uint32_t (&v)[FwdGeom<DT, M, R>::NI][FwdGeom<DT, M, R>::DW], int r0 = 0) {
+  using G = FwdGeom<DT, M, R>;
   const int rsub = lane / G::LPR, col = lane % G::LPR;
 #pragma unroll
   for (int p = 0; p < G::NI; ++p) {
-    const int32_t s = W.nbr[buf][p * G::RPI + rsub].slot;
+    const int32_t s = W.nbr[buf][r0 + p * G::RPI + rsub].slot;
     const char* src = tb + (size_t)(s >= 0 ? s : 0) * G::RB + col * G::BPL;
     if constexpr (G::DW == 1) {
       v[p][0] = s >= 0 ? *reinterpret_cast<const uint32_t*>(src) : 0u;
@@ -802,18 +830,16 @@ __device__ __forceinline__ void fwd_issue(const char* __restrict__ tb, const Wav
   }
 }
 
-template <int DT, int M>
-__device__ __forceinline__ void fwd_consume(const WaveLds& W, int buf, int lane, int64_t l,
-                                            const uint32_t (&v)[FwdGeom<DT, M>::NI][FwdGeom<DT, M>::DW],
-                                            void* __restrict__ out) {
-  using G = FwdGeom<DT, M>;
-  const int rsub = lane / G::LPR, col = lane % G::LPR;
-  float acc[G::EPL];
-#pragma unroll
-  for (int e = 0; e < G::EPL; ++e) acc[e] = 0.0f;
+// acc += sum over the rows r0 .. r0 + R of w_j * v_j (this lane's columns).
+template <int DT, int M, int KS, int R = NB>
+__device__ __forceinline__ void fwd_accumulate(const WaveLds<KS>& W, int buf, int lane,
+                                               const uint32_t (&v)[FwdGeom<DT, M, R>::NI][FwdGeom<DT, M, R>::DW],
+                                               float (&acc)[FwdGeom<DT, M, R>::EPL], int r0 = 0) {
+  using G = FwdGeom<DT, M, R>;
+  const int rsub = lane / G::LPR;
 #pragma unroll
   for (int p = 0; p < G::NI; ++p) {
-    const float w = W.wgt[buf][p * G::RPI + rsub];
+    const float w = W.wgt[buf][r0 + p * G::RPI + rsub];
     if constexpr (DT == LRAM_F32) {
 #pragma unroll
       for (int e = 0; e < G::EPL; ++e) acc[e] = fmaf(w, __uint_as_float(v[p][e]), acc[e]);
@@ -825,6 +851,14 @@ __device__ __forceinline__ void fwd_consume(const WaveLds& W, int buf, int lane,
       }
     }
   }
+}
+
+// Sums the row groups of the wave (xor shuffles) and writes out[l] once.
+template <int DT, int M>
+__device__ __forceinline__ void fwd_store(int lane, int64_t l, float (&acc)[FwdGeom<DT, M>::EPL],
+                                          void* __restrict__ out) {
+  using G = FwdGeom<DT, M>;
+  const int rsub = lane / G::LPR, col = lane % G::LPR;
 #pragma unroll
   for (int mask = G::LPR; mask < WAVE; mask <<= 1)
 #pragma unroll
@@ -842,6 +876,17 @@ __device__ __forceinline__ void fwd_consume(const WaveLds& W, int buf, int lane,
   }
 }
 
+template <int DT, int M>
+__device__ __forceinline__ void fwd_consume(const WaveLds<NB>& W, int buf, int lane, int64_t l,
+                                            const uint32_t (&v)[FwdGeom<DT, M>::NI][FwdGeom<DT, M>::DW],
+                                            void* __restrict__ out) {
+  float acc[FwdGeom<DT, M>::EPL];
+#pragma unroll
+  for (int e = 0; e < FwdGeom<DT, M>::EPL; ++e) acc[e] = 0.0f;
+  fwd_accumulate<DT, M, NB>(W, buf, lane, v, acc);
+  fwd_store<DT, M>(lane, l, acc, out);
+}
+
 // TH: the input is the activation layer's z [L][16] instead of q [L][8]; the
 // scale s is folded into the weights by the search.
 template <int DT, int M, bool TH>
@@ -851,20 +896,51 @@ __global__ void __launch_bounds__(THREADS) k_forward(const float* __restrict__ q
   __shared__ SearchLds<WAVE> S;
   WaveCtx c;
   if (!wave_ctx(P, c)) return;
-  Search srch(P, S.tab, S.wave[c.wave], c.wave, c.lane);
-  WaveLds& W = S.wave[c.wave];
+  Search<NB> srch(P, S.tab, S.wave[c.wave], c.wave, c.lane);
+  WaveLds<NB>& W = S.wave[c.wave];
   Frame* FR = S.frames[c.wave];
   phase_a<TH>(q, c.base, c.nl, P, FR, c.lane);
   const char* tb = reinterpret_cast<const char*>(table);
   uint32_t v[G::NI][G::DW];
   srch.run(FR[0], read_sel(FR[0]), 0);
-  fwd_issue<DT, M>(tb, W, 0, c.lane, v);
+  fwd_issue<DT, M, NB>(tb, W, 0, c.lane, v);
   for (int t = 0; t < c.nl; ++t) {
     const int buf = t & 1;
     // search lookup t+1 while the rows of lookup t are in flight
     if (t + 1 < c.nl) srch.run(FR[t + 1], read_sel(FR[t + 1]), buf ^ 1);
     fwd_consume<DT, M>(W, buf, c.lane, c.base + t, v, out);
-    if (t + 1 < c.nl) fwd_issue<DT, M>(tb, W, buf ^ 1, c.lane, v);
+    if (t + 1 < c.nl) fwd_issue<DT, M, NB>(tb, W, buf ^ 1, c.lane, v);
+  }
+}
+
+// Forward with lists of KS != 32 neighbours (the variable-k and untruncated
+// lookups): per lookup, the rows are gathered in chunks of up to 32, only as
+// many chunks as the lookup has neighbours.
+template <int DT, int M, int KS>
+__global__ void __launch_bounds__(THREADS) k_forward_k(const float* __restrict__ q, Params P,
+                                                       const void* __restrict__ table, void* __restrict__ out) {
+  constexpr int R = chunk_rows<KS>();
+  using G = FwdGeom<DT, M, R>;
+  __shared__ SearchLds<WAVE, KS> S;
+  WaveCtx c;
+  if (!wave_ctx(P, c)) return;
+  Search<KS> srch(P, S.tab, S.wave[c.wave], c.wave, c.lane);
+  WaveLds<KS>& W = S.wave[c.wave];
+  Frame* FR = S.frames[c.wave];
+  phase_a<false>(q, c.base, c.nl, P, FR, c.lane);
+  const char* tb = reinterpret_cast<const char*>(table);
+  for (int t = 0; t < c.nl; ++t) {
+    const int count = srch.run(FR[t], read_sel(FR[t]), 0);
+    float acc[G::EPL];
+#pragma unroll
+    for (int e = 0; e < G::EPL; ++e) acc[e] = 0.0f;
+    for (int r0 = 0; r0 < count; r0 += R) {
+      uint32_t v[G::NI][G::DW];
+      fwd_issue<DT, M, KS, R>(tb, W, 0, c.lane, v, r0);
+      fwd_accumulate<DT, M, KS, R>(W, 0, c.lane, v, acc, r0);
+    }
+    fwd_store<DT, M>(c.lane, c.base + t, acc, out);
+    wave_lds_sync();
   }
 }
 
@@ -873,14 +949,15 @@ __global__ void __launch_bounds__(THREADS) k_forward(const float* __restrict__ q
 
 // Value-gradient scatter of one lookup: M consecutive lanes own one gradient
 // row, so each atomic instruction covers 64/M whole rows.
-template <int M>
-__device__ __forceinline__ void scatter_atomic(const WaveLds& W, const float* __restrict__ gout, int64_t l,
-                                               float* __restrict__ gtab, int lane) {
+template <int M, int KS>
+__device__ __forceinline__ void scatter_atomic(const WaveLds<KS>& W, int count, const float* __restrict__ gout,
+                                               int64_t l, float* __restrict__ gtab, int lane) {
   constexpr int RA = WAVE / M;
   const int col = lane % M;
   const float gc = gout[(size_t)l * M + col];
+  const int kend = KS == NB ? NB / RA : (min(count, KS) + RA - 1) / RA;
 #pragma unroll 4
-  for (int k = 0; k < NB / RA; ++k) {
+  for (int k = 0; k < kend; ++k) {
     const int j = k * RA + lane / M;
     const int32_t s = W.nbr[0][j].slot;
     if (s >= 0) unsafeAtomicAdd(gtab + (size_t)s * M + col, W.wgt[0][j] * gc);
@@ -895,18 +972,19 @@ __device__ __forceinline__ void scatter_atomic(const WaveLds& W, const float* __
 //   dL/da_i = dL/ds s^2 a_i / r_i^3 - dL/dq_i c_i b_i / r_i^2,
 //   dL/db_i = dL/ds s^2 b_i / r_i^3 + dL/dq_i c_i a_i / r_i^2,
 // written to gq[l][16] (zero where s = 0); zin is z.
-template <int DT, int M, bool TH>
-__device__ __forceinline__ void grad_query(const Frame& F, const WaveLds& W, const Tables& T, int count,
+template <int DT, int M, bool TH, int KS>
+__device__ __forceinline__ void grad_query(const Frame& F, const WaveLds<KS>& W, const Tables& T, int count,
                                            const char* __restrict__ tb, const float* __restrict__ gout, int64_t l,
                                            int lane, float* __restrict__ gq, const float* __restrict__ zin,
                                            const Params& P) {
-  using G = RowGeom<DT, M>;
+  constexpr int R = chunk_rows<KS>();  // rows per chunk of the row loop
+  using G = RowGeom<DT, M, R>;
   constexpr int ICOORD = G::LPR >= 8 ? 1 : 8 / G::LPR;  // query coordinates per lane
   const int rsub = lane / G::LPR, ch = lane % G::LPR;
-  float dq[ICOORD];
+  double dq[ICOORD];
   double dls = 0.0;  // dL/ds (TH)
 #pragma unroll
-  for (int k = 0; k < ICOORD; ++k) dq[k] = 0.0f;
+  for (int k = 0; k < ICOORD; ++k) dq[k] = 0.0;
   if (count > 0) {
     float g[G::EPC];
     const float* gp = gout + (size_t)l * M + ch * G::EPC;
@@ -921,43 +999,34 @@ __device__ __forceinline__ void grad_query(const Frame& F, const WaveLds& W, con
     for (int k = 0; k < ICOORD; ++k) {
       lsel[k] = F.sel[(ch + k * G::LPR) & 7];
     }
+    for (int r0 = 0; r0 < (KS == NB ? 1 : count); r0 += R) {
     uint4 v[G::NP];
     int32_t sl[G::NP];
 #pragma unroll
     for (int p = 0; p < G::NP; ++p) {
-      sl[p] = W.nbr[0][p * G::RPP + rsub].slot;
+      sl[p] = W.nbr[0][r0 + p * G::RPP + rsub].slot;
       v[p] = sl[p] >= 0 ? *reinterpret_cast<const uint4*>(tb + (size_t)sl[p] * G::RB + ch * 16)
                         : make_uint4(0, 0, 0, 0);
     }
 #pragma unroll
     for (int p = 0; p < G::NP; ++p) {
-      const int j = p * G::RPP + rsub;
+      const int j = r0 + p * G::RPP + rsub;
       float f[G::EPC];
       unpack16<DT, G::EPC>(v[p], f);
-      // <G, v_j>: this lane's chunk, then a sum over the LPR lanes of the row.
-      // Behind the activation layer it is formed in fp64 (fp32 x fp32
-      // products are exact there): dL/ds = sum_j w_j <G, v_j> can cancel
-      // deeply (at a lattice point it is one dot product and dq = 0), and it
-      // then carries the whole gradient of the lookup.
-      float pd;
+      // <G, v_j>: this lane's chunk, then a sum over the LPR lanes of the row,
+      // in fp64 (fp32 x fp32 products are exact there).  Next to a lattice
+      // point one term carries all of dq (and behind the activation layer
+      // dL/ds is sum_j w_j <G, v_j>), so a cancelling fp32 dot product would
+      // become the relative error of the whole gradient.
       double pd64 = 0.0;
-      if constexpr (!TH) {
-        pd = 0.0f;
 #pragma unroll
-        for (int e = 0; e < G::EPC; ++e) pd = fmaf(g[e], f[e], pd);
+      for (int e = 0; e < G::EPC; ++e) pd64 = fma((double)g[e], (double)f[e], pd64);
 #pragma unroll
-        for (int mask = 1; mask < G::LPR; mask <<= 1) pd += __shfl_xor(pd, mask);
-      } else {
-#pragma unroll
-        for (int e = 0; e < G::EPC; ++e) pd64 = fma((double)g[e], (double)f[e], pd64);
-#pragma unroll
-        for (int mask = 1; mask < G::LPR; mask <<= 1) pd64 += __shfl_xor(pd64, mask);
-        pd = (float)pd64;
-      }
+      for (int mask = 1; mask < G::LPR; mask <<= 1) pd64 += __shfl_xor(pd64, mask);
       if (sl[p] >= 0) {
         const Nbr n = W.nbr[0][j];
         const float u = 1.0f - __uint_as_float(n.dbits) * 0.125f;
-        const float a = -2.0f * u * u * u * pd;
+        const double a = -2.0 * (double)(u * u * u) * pd64;
         if constexpr (TH) {
           const float u2 = u * u;
           dls = fma((double)(u2 * u2), pd64, dls);
@@ -967,11 +1036,12 @@ __device__ __forceinline__ void grad_query(const Frame& F, const WaveLds& W, con
           const int i = ch + k * G::LPR;
           if (i < 8) {
             const uint32_t ab = __builtin_amdgcn_perm(n.hi, n.lo, lsel[k]);
-            dq[k] = fmaf(a, lds_f32(T.et, ab + 256u * i), dq[k]);
+            dq[k] = fma(a, (double)lds_f32(T.et, ab + 256u * i), dq[k]);
           }
         }
       }
     }
+    }  // chunks of R rows
   }
 #pragma unroll
   for (int mask = G::LPR; mask < WAVE; mask <<= 1) {
@@ -985,7 +1055,7 @@ __device__ __forceinline__ void grad_query(const Frame& F, const WaveLds& W, con
       const int i = ch + k * G::LPR;
       if (i >= 8) continue;
       if constexpr (!TH) {
-        gq[l * 8 + i] = dq[k];
+        gq[l * 8 + i] = (float)dq[k];
       } else {
         double ci = P.cK[0];
 #pragma unroll
@@ -997,7 +1067,7 @@ __device__ __forceinline__ void grad_query(const Frame& F, const WaveLds& W, con
           const double a = ab.x, b = ab.y;
           const double r2 = a * a + b * b;
           const double r3 = r2 * sqrt(r2);
-          const double ds = dls * sc * sc, dqs = (double)dq[k] * sc * ci;
+          const double ds = dls * sc * sc, dqs = dq[k] * sc * ci;
           ga = ds * a / r3 - dqs * b / r2;
           gb = ds * b / r3 + dqs * a / r2;
         }
@@ -1011,18 +1081,19 @@ __device__ __forceinline__ void grad_query(const Frame& F, const WaveLds& W, con
 // atomics (EMIT = false), or emitted as (location, (lookup, w_j)) pairs for
 // the sorted segmented reduction (EMIT = true; padding gets the key N, which
 // sorts last).
-template <int DT, int M, bool EMIT, bool TH>
+template <int DT, int M, bool EMIT, bool TH, int KS = NB>
 __global__ void __launch_bounds__(THREADS) k_backward(const float* __restrict__ q, Params P,
                                                       const void* __restrict__ table,
                                                       const float* __restrict__ gout, float* __restrict__ gtab,
                                                       float* __restrict__ gq, uint32_t* __restrict__ pair_key,
                                                       uint2* __restrict__ pair_val) {
-  __shared__ SearchLds<WAVE> S;
+  static_assert(!EMIT || KS == NB, "the sorted scatter takes lists of 32");
+  __shared__ SearchLds<WAVE, KS> S;
   WaveCtx c;
   if (!wave_ctx(P, c)) return;
   const int lane = c.lane;
-  Search srch(P, S.tab, S.wave[c.wave], c.wave, lane);
-  WaveLds& W = S.wave[c.wave];
+  Search<KS> srch(P, S.tab, S.wave[c.wave], c.wave, lane);
+  WaveLds<KS>& W = S.wave[c.wave];
   Frame* FR = S.frames[c.wave];
   phase_a<TH>(q, c.base, c.nl, P, FR, lane);
   const char* tb = reinterpret_cast<const char*>(table);
@@ -1031,8 +1102,8 @@ __global__ void __launch_bounds__(THREADS) k_backward(const float* __restrict__ 
     const Sel sel = read_sel(F);
     const int count = srch.run(F, sel, 0);
     const int64_t l = c.base + t;
-    if (!EMIT && gtab && count > 0) scatter_atomic<M>(W, gout, l, gtab, lane);
-    if (gq) grad_query<DT, M, TH>(F, W, S.tab, count, tb, gout, l, lane, gq, q, P);
+    if (!EMIT && gtab && count > 0) scatter_atomic<M, KS>(W, count, gout, l, gtab, lane);
+    if (gq) grad_query<DT, M, TH, KS>(F, W, S.tab, count, tb, gout, l, lane, gq, q, P);
     if (EMIT && gtab && lane < NB) {
       const int32_t s = W.nbr[0][lane].slot;
       pair_key[l * NB + lane] = s >= 0 ? (uint32_t)s : P.N;
@@ -1411,8 +1482,8 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
     const int64_t base = bbase + (int64_t)wave * P.lpw;
     const int nl = (int)max<int64_t>(0, min<int64_t>(P.lpw, P.L - base));
     if (nl > 0) {
-      Search srch(P, S.b.search.tab, S.b.search.wave[wave], wave, lane);
-      WaveLds& W = S.b.search.wave[wave];
+      Search<NB> srch(P, S.b.search.tab, S.b.search.wave[wave], wave, lane);
+      WaveLds<NB>& W = S.b.search.wave[wave];
       Frame* FR = S.b.search.frames[wave];
       const uint32_t my_l = phase_a_perm<TH>(q, perm, base, nl, P, FR, lane);
       const char* tb = reinterpret_cast<const char*>(table);
@@ -1421,8 +1492,8 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
         const Sel sel = read_sel(F);
         const int count = srch.run(F, sel, 0);
         const int64_t l = (int64_t)__builtin_amdgcn_readlane(my_l, i);
-        if (!merge && count > 0) scatter_atomic<M>(W, gout, l, gtab, lane);
-        if (gq) grad_query<DT, M, TH>(F, W, S.b.search.tab, count, tb, gout, l, lane, gq, q, P);
+        if (!merge && count > 0) scatter_atomic<M, NB>(W, count, gout, l, gtab, lane);
+        if (gq) grad_query<DT, M, TH, NB>(F, W, S.b.search.tab, count, tb, gout, l, lane, gq, q, P);
         if (merge && lane < NB) {
           const int pidx = (wave * P.lpw + i) * NB + lane;
           S.a.pairs.loc[pidx] = W.nbr[0][lane].slot;
@@ -1789,6 +1860,44 @@ struct BwdSortedLaunch {
   }
 };
 
+// List width for k neighbours (k = LRAM_ALL: the whole support), 0 if k is not offered.
+int list_width(int32_t k) {
+  return k == LRAM_ALL ? KALL : ((k == 16 || k == 32 || k == 64) ? k : 0);
+}
+
+template <int DT, int M>
+struct FwdKLaunch {
+  static int go(const float* q, const Params& P, const void* table, void* out, int width, hipStream_t s) {
+    const dim3 g(grid_for(P)), b(THREADS);
+    switch (width) {
+      case 16: hipLaunchKernelGGL((k_forward_k<DT, M, 16>), g, b, 0, s, q, P, table, out); break;
+      case 64: hipLaunchKernelGGL((k_forward_k<DT, M, 64>), g, b, 0, s, q, P, table, out); break;
+      case KALL: hipLaunchKernelGGL((k_forward_k<DT, M, KALL>), g, b, 0, s, q, P, table, out); break;
+      default: hipLaunchKernelGGL((k_forward<DT, M, false>), g, b, 0, s, q, P, table, out); break;
+    }
+    return launched();
+  }
+};
+
+template <int DT, int M>
+struct BwdKLaunch {
+  static int go(const float* q, const Params& P, const void* table, const float* g, float* gt, float* gq, int width,
+                hipStream_t s) {
+    const dim3 gr(grid_for(P)), b(THREADS);
+    uint32_t* nk = nullptr;
+    uint2* nv = nullptr;
+    switch (width) {
+      case 16: hipLaunchKernelGGL((k_backward<DT, M, false, false, 16>), gr, b, 0, s, q, P, table, g, gt, gq, nk, nv); break;
+      case 64: hipLaunchKernelGGL((k_backward<DT, M, false, false, 64>), gr, b, 0, s, q, P, table, g, gt, gq, nk, nv); break;
+      case KALL:
+        hipLaunchKernelGGL((k_backward<DT, M, false, false, KALL>), gr, b, 0, s, q, P, table, g, gt, gq, nk, nv);
+        break;
+      default: hipLaunchKernelGGL((k_backward<DT, M, false, false, NB>), gr, b, 0, s, q, P, table, g, gt, gq, nk, nv); break;
+    }
+    return launched();
+  }
+};
+
 int forward_impl(const float* in, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype, int64_t N,
                  int32_t m, void* out, bool th, hipStream_t stream) {
   int64_t L;
@@ -1872,7 +1981,7 @@ int lram_neighbors(const float* q, int64_t B, int64_t H, const int32_t K[8], int
   if (rc) return rc;
   if (L == 0) return LRAM_OK;
   if (!slot || !w) return LRAM_EINVAL;
-  hipLaunchKernelGGL(k_neighbors, dim3(grid_for(P)), dim3(THREADS), 0, (hipStream_t)stream, q, P, slot, w, d2);
+  hipLaunchKernelGGL(k_neighbors<NB>, dim3(grid_for(P)), dim3(THREADS), 0, (hipStream_t)stream, q, P, slot, w, d2);
   return launched();
 }
 
@@ -1931,6 +2040,61 @@ int lram_theta_backward(const float* z, int64_t B, int64_t H, const int32_t K[8]
                         void* workspace, size_t ws_bytes, void* stream) {
   return backward_impl(z, B, H, K, table, dtype, N, m, grad_out, grad_table, grad_z, mode, workspace, ws_bytes,
                        true, (hipStream_t)stream);
+}
+
+int lram_neighbors_k(const float* q, int64_t B, int64_t H, const int32_t K[8], int32_t k, int32_t* slot, float* w,
+                     float* d2, void* stream) {
+  const int width = list_width(k);
+  if (!width) return LRAM_EINVAL;
+  int64_t L;
+  Params P;
+  int rc = check_common(q, B, H, K, &L, &P);
+  if (rc) return rc;
+  if (L == 0) return LRAM_OK;
+  if (!slot || !w) return LRAM_EINVAL;
+  const dim3 g(grid_for(P)), b(THREADS);
+  hipStream_t s = (hipStream_t)stream;
+  switch (width) {
+    case 16: hipLaunchKernelGGL(k_neighbors<16>, g, b, 0, s, q, P, slot, w, d2); break;
+    case 64: hipLaunchKernelGGL(k_neighbors<64>, g, b, 0, s, q, P, slot, w, d2); break;
+    case KALL: hipLaunchKernelGGL(k_neighbors<KALL>, g, b, 0, s, q, P, slot, w, d2); break;
+    default: hipLaunchKernelGGL(k_neighbors<NB>, g, b, 0, s, q, P, slot, w, d2); break;
+  }
+  return launched();
+}
+
+int lram_forward_k(const float* q, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
+                   int64_t N, int32_t m, int32_t k, void* out, void* stream) {
+  const int width = list_width(k);
+  if (!width) return LRAM_EINVAL;
+  int64_t L;
+  Params P;
+  int rc = check_common(q, B, H, K, &L, &P);
+  if (rc) return rc;
+  rc = check_table(table, dtype, N, m, P, L);
+  if (rc) return rc;
+  if (L == 0) return LRAM_OK;
+  if (!out || (reinterpret_cast<uintptr_t>(out) & 15)) return LRAM_EINVAL;
+  return dispatch<FwdKLaunch>(dtype, m, q, P, table, out, width, (hipStream_t)stream);
+}
+
+int lram_backward_k(const float* q, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
+                    int64_t N, int32_t m, int32_t k, const float* grad_out, float* grad_table, float* grad_q,
+                    void* stream) {
+  const int width = list_width(k);
+  if (!width) return LRAM_EINVAL;
+  int64_t L;
+  Params P;
+  int rc = check_common(q, B, H, K, &L, &P);
+  if (rc) return rc;
+  rc = check_table(table, dtype, N, m, P, L);
+  if (rc) return rc;
+  if (L == 0) return LRAM_OK;
+  if (!grad_out || (reinterpret_cast<uintptr_t>(grad_out) & 15)) return LRAM_EINVAL;
+  if (!grad_table && !grad_q) return LRAM_EINVAL;
+  if (grad_table && (reinterpret_cast<uintptr_t>(grad_table) & 15)) return LRAM_EINVAL;
+  if (grad_q && (reinterpret_cast<uintptr_t>(grad_q) & 15)) return LRAM_EINVAL;
+  return dispatch<BwdKLaunch>(dtype, m, q, P, table, grad_out, grad_table, grad_q, width, (hipStream_t)stream);
 }
 
 }  // extern "C"

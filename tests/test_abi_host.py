@@ -111,6 +111,16 @@ def test_theta_validation(lib):
     assert lib.lram_theta_backward(FAKE, 4, 1, K4, FAKE, 0, 4 ** 8, 32, FAKE, FAKE, FAKE, 2, None, 0, None) == 4
 
 
+def test_variable_k_validation(lib):
+    assert lib.lram_forward_k(FAKE, 4, 1, K4, FAKE, 0, 4 ** 8, 32, 48, FAKE, None) == 1   # k not offered
+    assert lib.lram_forward_k(FAKE, 4, 1, K4, FAKE, 0, 4 ** 8, 32, -1, FAKE, None) == 1
+    assert lib.lram_neighbors_k(FAKE, 4, 1, K4, 128, FAKE, FAKE, None, None) == 1
+    assert lib.lram_neighbors_k(FAKE, 4, 1, (ctypes.c_int32 * 8)(*([5] * 8)), 0, FAKE, FAKE, None, None) == 2
+    assert lib.lram_backward_k(FAKE, 4, 1, K4, FAKE, 0, 4 ** 8, 32, 16, None, FAKE, FAKE, None) == 1
+    assert lib.lram_backward_k(FAKE, 4, 1, K4, FAKE, 0, 4 ** 8, 40, 16, FAKE, FAKE, FAKE, None) == 3
+    assert lib.lram_forward_k(None, 0, 1, K4, None, 0, 4 ** 8, 32, 0, None, None) == 0
+
+
 def test_auto_mode(lib):
     r = ctypes.c_int(-1)
     assert lib.lram_scatter_mode_resolved(4, 1, 3, ctypes.byref(r)) == 0 and r.value == 0        # small: atomic
