@@ -117,6 +117,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-compare", action="store_true", help="skip timing the other scatter modes")
     ap.add_argument("--no-theta", action="store_true", help="skip timing the activation layer path")
+    ap.add_argument("--no-k", action="store_true", help="skip timing the variable-k lookups")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (HBM counter calibration)")
     args = ap.parse_args()
@@ -239,6 +240,34 @@ def main():
         log("activation layer + lookup: forward %.3f ms, backward %.3f ms" % (tf, tb))
         del z, gz, wsp
 
+    # coverage vs bandwidth: the same lookups truncated to k = 16, 32, 64 or
+    # untruncated (not part of `value`); coverage = mean share of the kernel's
+    # total weight on a 65,536-lookup sample
+    by_k = None
+    if not args.no_k:
+        by_k = {}
+        qs = q.reshape(-1, 8)[:65536]
+        tot_all = lram.neighbors(qs, w.K, want_d2=False, k=lram.ALL)[1].double().sum(1)
+        for kk in (16, 32, 64, lram.ALL):
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            lram.forward(q, table, w.K, out=out, k=kk)
+            lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, k=kk, mode="atomic")
+            torch.cuda.synchronize()
+            e[0].record(stream)
+            for _ in range(3):
+                lram.forward(q, table, w.K, out=out, k=kk)
+            e[1].record(stream)
+            for _ in range(3):
+                lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, k=kk, mode="atomic")
+            e[2].record(stream)
+            torch.cuda.synchronize()
+            cov = (lram.neighbors(qs, w.K, want_d2=False, k=kk)[1].double().sum(1) / tot_all).mean().item()
+            name = "all" if kk == lram.ALL else str(kk)
+            by_k[name] = {"fwd_ms": e[0].elapsed_time(e[1]) / 3, "bwd_atomic_ms": e[1].elapsed_time(e[2]) / 3,
+                          "coverage": cov}
+            log("k=%s: forward %.3f ms, backward (atomic) %.3f ms, weight coverage %.6f" % (
+                name, by_k[name]["fwd_ms"], by_k[name]["bwd_atomic_ms"], cov))
+
     st = 4 if w.dtype == "f32" else 2
     L = w.L
     fwd_bytes = L * (32 + w.m * st) + U * w.m * st
@@ -276,6 +305,7 @@ def main():
         "bwd_ms_by_scatter": by_scatter,
         "distinct_rows": U,
         "theta": theta,
+        "by_k": by_k,
         "roofline": {"kernel": kname, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "bytes_per_launch": kbytes, "requested_bytes_per_launch": kreq,
