@@ -118,6 +118,7 @@ def main():
     ap.add_argument("--no-compare", action="store_true", help="skip timing the other scatter modes")
     ap.add_argument("--no-theta", action="store_true", help="skip timing the activation layer path")
     ap.add_argument("--no-k", action="store_true", help="skip timing the variable-k lookups")
+    ap.add_argument("--no-subnetwork", action="store_true", help="skip timing the memory subnetwork slice")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (HBM counter calibration)")
     args = ap.parse_args()
@@ -319,7 +320,46 @@ def main():
         log("cpu baseline (oracle) ...")
         res["cpu_baseline"] = cpu_baseline(oracle, W, w, q_np, table, G, args.cpu_seconds, torch)
         log("cpu baseline done")
+    if not args.no_subnetwork:
+        del table, gtab, G, out, gq, q
+        torch.cuda.empty_cache()
+        res["memory_subnetwork"] = time_subnetwork(torch, lram, log)
     print(json.dumps(res), flush=True)
+
+
+def time_subnetwork(torch, lram, log, widths=(2048, 3072, 4096, 6144, 8192, 12288), tokens=8192, K=(10,) * 8):
+    """Inference time per vector of the memory subnetwork (dense w -> w, batch
+    norm, theta with h = w/16 heads of m = 64, dense 4w -> w) at the widths of
+    the paper's timing table, bf16 dense layers and table, one shared table of
+    prod K = 1e8 locations (12.8 GB), a batch of 8192 vectors (32 x 256 tokens)."""
+    from paper_2107_03474_amd.memory_layer import MemorySubnetwork, M_VALUE
+
+    N = int(np.prod(K))
+    table = torch.empty((N, M_VALUE), dtype=torch.bfloat16, device="cuda")
+    for s in range(0, N, 1 << 22):
+        table[s:s + (1 << 22)] = torch.randn((min(1 << 22, N - s), M_VALUE), device="cuda") * 0.02
+    out = {"tokens": tokens, "K": list(K), "dtype": "bf16 dense and table, fp32 accumulate", "us_per_vector": {}}
+    for wd in widths:
+        net = MemorySubnetwork(wd, K, dtype=torch.bfloat16, table=table).eval()
+        x = torch.randn((tokens, wd), device="cuda", dtype=torch.bfloat16)
+        with torch.no_grad():
+            for _ in range(2):
+                net(x)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(5):
+                net(x)
+            e1.record()
+            torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) / 5 * 1e3 / tokens
+        out["us_per_vector"][str(wd)] = us
+        log("memory subnetwork w=%d: %.3f us per vector (%d lookups per batch)" % (wd, us, tokens * wd // 16))
+        del net, x
+        torch.cuda.empty_cache()
+    del table
+    torch.cuda.empty_cache()
+    return out
 
 
 if __name__ == "__main__":

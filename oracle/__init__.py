@@ -240,9 +240,9 @@ def theta_forward(nb: dict, rows: np.ndarray, s: np.ndarray) -> np.ndarray:
     return np.asarray(s, np.float64)[..., None] * forward(nb, rows)
 
 
-def theta_grad_table_rows(nb: dict, s: np.ndarray, G: np.ndarray):
+def theta_grad_table_rows(nb: dict, s: np.ndarray, G: np.ndarray, weights: str = "w64"):
     """Value-table gradient of <G, theta>: the lookup's with G scaled by s."""
-    return grad_table_rows(nb, np.asarray(G, np.float64) * np.asarray(s, np.float64)[..., None])
+    return grad_table_rows(nb, np.asarray(G, np.float64) * np.asarray(s, np.float64)[..., None], weights)
 
 
 def theta_grad_z(z: np.ndarray, K, nb: dict, rows: np.ndarray, s: np.ndarray, G: np.ndarray) -> np.ndarray:
