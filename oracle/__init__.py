@@ -272,3 +272,45 @@ def theta_grad_z(z: np.ndarray, K, nb: dict, rows: np.ndarray, s: np.ndarray, G:
     out[..., 0::2] = np.where(ok[..., None], ga, 0.0)
     out[..., 1::2] = np.where(ok[..., None], gb, 0.0)
     return out
+
+
+# ---------------------------------------------------------------------------
+# Training-side companions: the optimiser step on the memory table (Sec. 3.2:
+# Adam, learning rate 1e-3 for the memory parameters) and the access
+# statistics of Sec. 4.3 (Table 5).
+
+def sparse_adam(table, grad, exp_avg, exp_avg_sq, step, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8):
+    """One Adam step (Kingma & Ba, Algorithm 1: bias-corrected moments, eps
+    outside the square root) on the rows of the table whose gradient row is not
+    identically zero; the other rows keep their values and moments (the lazy,
+    sparse form).  fp64; returns new (table, exp_avg, exp_avg_sq)."""
+    V = np.array(table, np.float64)
+    g = np.asarray(grad, np.float64)
+    m1 = np.array(exp_avg, np.float64)
+    m2 = np.array(exp_avg_sq, np.float64)
+    rows = np.any(g != 0, axis=1)
+    m1[rows] = beta1 * m1[rows] + (1 - beta1) * g[rows]
+    m2[rows] = beta2 * m2[rows] + (1 - beta2) * g[rows] ** 2
+    mh = m1[rows] / (1 - beta1 ** step)
+    vh = m2[rows] / (1 - beta2 ** step)
+    V[rows] = V[rows] - lr * mh / (np.sqrt(vh) + eps)
+    return V, m1, m2
+
+
+def access_histogram(nb: dict, N: int) -> np.ndarray:
+    """Weighted access count of every location: sum of the kernel weights of
+    the (lookup, neighbour) pairs that read it (fp64)."""
+    s = nb["slot"].reshape(-1)
+    w = nb["w64"].reshape(-1)
+    ok = s >= 0
+    return np.bincount(s[ok], weights=w[ok], minlength=N).astype(np.float64)
+
+
+def access_stats(hist: np.ndarray):
+    """(fraction of locations accessed, KL divergence of the weighted access
+    distribution from uniform) -- the two columns of Table 5."""
+    h = np.asarray(hist, np.float64)
+    N = h.size
+    tot = h.sum()
+    p = h[h > 0] / tot
+    return float((h > 0).mean()), float(np.sum(p * np.log(p * N)))
