@@ -119,6 +119,7 @@ def main():
     ap.add_argument("--no-theta", action="store_true", help="skip timing the activation layer path")
     ap.add_argument("--no-k", action="store_true", help="skip timing the variable-k lookups")
     ap.add_argument("--no-subnetwork", action="store_true", help="skip timing the memory subnetwork slice")
+    ap.add_argument("--no-training", action="store_true", help="skip the access statistics and the Adam step")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (HBM counter calibration)")
     args = ap.parse_args()
@@ -324,7 +325,52 @@ def main():
         del table, gtab, G, out, gq, q
         torch.cuda.empty_cache()
         res["memory_subnetwork"] = time_subnetwork(torch, lram, log)
+    if not args.no_training:
+        res["training"] = time_training(torch, lram, W, log)
     print(json.dumps(res), flush=True)
+
+
+def time_training(torch, lram, W, log, batches=16):
+    """The utilisation table's analogue and the optimiser step at the paper's
+    memory sizes (2^18, 2^20, 2^22 locations of m = 64 fp32): access share and
+    KL over `batches` synthetic batches of 8192 x 32 lookups (the queries of
+    the bench workload's Zipf/uniform mix on each torus), then one backward +
+    sparse Adam step per batch; Adam time and its HBM rate (grad scan + the
+    touched rows' moments, values and cleared gradient)."""
+    out = {}
+    for name, K in (("2^18", (4, 4, 4, 4, 4, 4, 8, 8)), ("2^20", (4, 4, 4, 4, 8, 8, 8, 8)),
+                    ("2^22", (4, 4, 8, 8, 8, 8, 8, 8))):
+        N = int(np.prod(K))
+        wl = W.Workload("stats", K, 64, "f32", 8192, 32, "zipf_mix", True, gmm_sigma=0.3, zipf_centres=4096,
+                        zipf_s=1.1)
+        table = torch.randn((N, 64), device="cuda") * 0.02
+        opt = lram.SparseAdam(table, lr=1e-3)
+        gtab = torch.zeros((N, 64), dtype=torch.float32, device="cuda")
+        hist = torch.zeros(N, dtype=torch.float32, device="cuda")
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        adam_ms, touched = 0.0, 0
+        for b in range(batches):
+            q = torch.from_numpy(W.queries(wl, seed=100 + b)).to("cuda")
+            lram.access_histogram(q, K, hist)
+            G = torch.randn((wl.B, wl.H, 64), device="cuda")
+            lram.backward(q, table, K, G, grad_table=gtab, want_grad_q=False)
+            if b == batches - 1:
+                touched = int((gtab != 0).any(1).sum().item())
+            ev[0].record()
+            opt.step(gtab)
+            ev[1].record()
+            torch.cuda.synchronize()
+            adam_ms += ev[0].elapsed_time(ev[1]) / batches
+        st = lram.access_stats(hist)
+        adam_bytes = N * 64 * 4 + touched * 64 * 4 * 7
+        out[name] = {"locations": N, "K": list(K), "lookups": batches * wl.L, "used": st["used"], "kl": st["kl"],
+                     "adam_ms": adam_ms, "adam_touched_rows": touched,
+                     "adam_GBps": adam_bytes / (adam_ms * 1e-3) / 1e9}
+        log("memory %s: used %.4f, KL %.3f over %d lookups; Adam step %.3f ms (%d touched rows, %.0f GB/s)" % (
+            name, st["used"], st["kl"], batches * wl.L, adam_ms, touched, out[name]["adam_GBps"]))
+        del table, opt, gtab, hist
+        torch.cuda.empty_cache()
+    return out
 
 
 def time_subnetwork(torch, lram, log, widths=(2048, 3072, 4096, 6144, 8192, 12288), tokens=8192, K=(10,) * 8):

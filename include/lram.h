@@ -141,6 +141,35 @@ int lram_backward(const float* q, int64_t B, int64_t H, const int32_t K[8], cons
                   void* workspace, size_t ws_bytes, void* stream);
 
 /*
+ * Training-side companions.
+ *
+ * lram_access_histogram -- hist[s] += sum of the kernel weights w_j of the
+ * (lookup, neighbour) pairs whose location is s (the weighted accesses of the
+ * utilisation table, Sec. 4.3); hist [N] fp32 device, accumulated (fp32 atomics).
+ *
+ * lram_access_stats -- from hist [N]: out (device, 4 doubles, 8-byte aligned,
+ * overwritten) = {fraction of locations with hist > 0, KL divergence of the
+ * distribution hist / sum(hist) from uniform (nats), sum(hist), number of
+ * locations with hist > 0}.  fp64 reductions.
+ *
+ * lram_sparse_adam -- one Adam step (Sec. 3.2 trains the memory with Adam,
+ * learning rate 1e-3; Algorithm 1 of Adam: m = b1 m + (1-b1) g,
+ * v = b2 v + (1-b2) g^2, table -= lr (m / (1-b1^step)) / (sqrt(v / (1-b2^step)) + eps))
+ * on the rows whose gradient row in grad [N][m] fp32 is not identically zero;
+ * other rows keep value and moments (the lazy, sparse form).  exp_avg and
+ * exp_avg_sq are [N][m] fp32 (zero-initialised by the caller), table is
+ * [N][m] in dtype (bf16: updated in fp32, rounded once).  grad rows that were
+ * used are cleared to zero.  step >= 1; lr, beta1, beta2, eps are host
+ * doubles: 1 - beta and the bias corrections 1 - beta^step are formed in fp64
+ * and rounded once (beta2 = 0.999 in fp32 would move 1 - beta2^step by
+ * 1e-5 relative); the per-entry arithmetic is fp32.
+ */
+int lram_access_histogram(const float* q, int64_t B, int64_t H, const int32_t K[8], float* hist, void* stream);
+int lram_access_stats(const float* hist, int64_t N, double* out, void* stream);
+int lram_sparse_adam(void* table, int dtype, int64_t N, int32_t m, float* grad, float* exp_avg, float* exp_avg_sq,
+                     int64_t step, double lr, double beta1, double beta2, double eps, void* stream);
+
+/*
  * Variable k and the untruncated lookup (Sec. 2.2 and 2.5: the sum over every
  * lattice point in the support; Sec. 2.6: the truncation to the closest k,
  * whose k = 32 is what every other entry point uses).  k is 16, 32, 64 or

@@ -297,11 +297,12 @@ def sparse_adam(table, grad, exp_avg, exp_avg_sq, step, lr=1e-3, beta1=0.9, beta
     return V, m1, m2
 
 
-def access_histogram(nb: dict, N: int) -> np.ndarray:
+def access_histogram(nb: dict, N: int, weights: str = "w64") -> np.ndarray:
     """Weighted access count of every location: sum of the kernel weights of
-    the (lookup, neighbour) pairs that read it (fp64)."""
+    the (lookup, neighbour) pairs that read it (fp64; ``weights`` as in
+    grad_table_rows)."""
     s = nb["slot"].reshape(-1)
-    w = nb["w64"].reshape(-1)
+    w = nb[weights].reshape(-1).astype(np.float64)
     ok = s >= 0
     return np.bincount(s[ok], weights=w[ok], minlength=N).astype(np.float64)
 

@@ -17,13 +17,14 @@ import os
 import threading
 from typing import Optional, Sequence, Tuple
 
+import numpy as np
 import torch  # noqa: F401  -- loads the HIP runtime liblram.so must share
 
 __all__ = ["neighbors", "forward", "backward", "backward_workspace_bytes", "lookup", "LramLookup",
            "library_path", "load", "LramError", "F32", "BF16", "SCATTER_ATOMIC", "SCATTER_SORTED",
            "SCATTER_MERGED", "SCATTER_AUTO", "resolved_mode", "NB",
            "theta_coords", "theta_forward", "theta_backward", "ThetaLookup", "theta", "ALL", "MAX_SUPPORT",
-           "list_width"]
+           "list_width", "access_histogram", "access_stats", "sparse_adam", "SparseAdam"]
 
 NB = 32
 F32, BF16 = 0, 1
@@ -74,6 +75,13 @@ def load():
             lib.lram_forward_k.restype = I
             lib.lram_backward_k.argtypes = [P, I64, I64, P, P, I, I64, I32, I32, P, P, P, P]
             lib.lram_backward_k.restype = I
+            lib.lram_access_histogram.argtypes = [P, I64, I64, P, P, P]
+            lib.lram_access_histogram.restype = I
+            lib.lram_access_stats.argtypes = [P, I64, P, P]
+            lib.lram_access_stats.restype = I
+            lib.lram_sparse_adam.argtypes = [P, I, I64, I32, P, P, P, I64, ctypes.c_double, ctypes.c_double,
+                                             ctypes.c_double, ctypes.c_double, P]
+            lib.lram_sparse_adam.restype = I
             lib.lram_theta_coords.argtypes = [P, I64, I64, P, P, P, P]
             lib.lram_theta_coords.restype = I
             lib.lram_theta_forward.argtypes = [P, I64, I64, P, P, I, I64, I32, P, P]
@@ -313,3 +321,54 @@ class ThetaLookup(torch.autograd.Function):
 
 def theta(z: torch.Tensor, table: torch.Tensor, K: Sequence[int], mode="auto") -> torch.Tensor:
     return ThetaLookup.apply(z, table, tuple(K), mode)
+
+
+# ---------------------------------------------------------------------------
+# Training-side companions: access statistics and the sparse Adam step.
+
+def access_histogram(q: torch.Tensor, K: Sequence[int], hist: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """hist [N] fp32 += the kernel weights of every (lookup, neighbour) pair at its location."""
+    lib = load()
+    B, H = _bh(q)
+    N = int(np.prod([int(k) for k in K]))
+    if hist is None:
+        hist = torch.zeros(N, dtype=torch.float32, device=q.device)
+    _check(lib.lram_access_histogram(_dev(q, "q", torch.float32), B, H, _K(K), _dev(hist, "hist", torch.float32),
+                                     _stream(q)))
+    return hist
+
+
+def access_stats(hist: torch.Tensor) -> dict:
+    """{used: fraction of locations accessed, kl: KL(access distribution || uniform),
+    total: summed weight, count: locations accessed} (synchronises to read them)."""
+    lib = load()
+    out = torch.empty(4, dtype=torch.float64, device=hist.device)
+    _check(lib.lram_access_stats(_dev(hist, "hist", torch.float32), hist.numel(), _dev(out, "out"), _stream(hist)))
+    v = out.cpu().tolist()
+    return {"used": v[0], "kl": v[1], "total": v[2], "count": int(round(v[3]))}
+
+
+def sparse_adam(table: torch.Tensor, grad: torch.Tensor, exp_avg: torch.Tensor, exp_avg_sq: torch.Tensor,
+                step: int, lr: float = 1e-3, betas=(0.9, 0.999), eps: float = 1e-8):
+    """One Adam step on the rows of ``table`` whose ``grad`` row is not all zero
+    (in place; those grad rows are cleared)."""
+    lib = load()
+    N, m = table.shape
+    _check(lib.lram_sparse_adam(_dev(table, "table"), _table_dtype(table), N, m, _dev(grad, "grad", torch.float32),
+                                _dev(exp_avg, "exp_avg", torch.float32), _dev(exp_avg_sq, "exp_avg_sq", torch.float32),
+                                int(step), float(lr), float(betas[0]), float(betas[1]), float(eps), _stream(table)))
+
+
+class SparseAdam:
+    """Adam state for one lattice memory table (the memory parameters of
+    Sec. 3.2, learning rate 1e-3): call ``step(grad)`` with the accumulated
+    fp32 gradient table; untouched rows keep value and moments."""
+
+    def __init__(self, table: torch.Tensor, lr: float = 1e-3, betas=(0.9, 0.999), eps: float = 1e-8):
+        self.table, self.lr, self.betas, self.eps, self.t = table, lr, betas, eps, 0
+        self.exp_avg = torch.zeros(table.shape, dtype=torch.float32, device=table.device)
+        self.exp_avg_sq = torch.zeros(table.shape, dtype=torch.float32, device=table.device)
+
+    def step(self, grad: torch.Tensor):
+        self.t += 1
+        sparse_adam(self.table, grad, self.exp_avg, self.exp_avg_sq, self.t, self.lr, self.betas, self.eps)

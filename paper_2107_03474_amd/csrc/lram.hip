@@ -22,6 +22,7 @@
 // No MFMA: the path is a gather / scatter bound by HBM, not a contraction.
 
 #include <hip/hip_runtime.h>
+#include <cmath>
 #include <stdint.h>
 
 #include <utility>
@@ -626,8 +627,8 @@ struct Search {
 #pragma unroll
       for (int k = 0; k < NS_STRICT; ++k)
         key[k] = (lane + WAVE * k < E8_NSTRICT) ? __float_as_uint(cand_d2(S.qt, lo[k], hi[k], sel)) : KEY_INF;
-      uint32_t thr, tie_key;
-      int need;
+      uint32_t thr = KEY_8, tie_key = KEY_INF;
+      int need = 0;
       bool suspect = true;
       if constexpr (KS != KALL) count = threshold_k_hist<NS_STRICT>(key, W.hist, lane, KS, thr, tie_key, need, suspect);
       if (!suspect) {
@@ -1619,6 +1620,110 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
 }
 
 // ---------------------------------------------------------------------------
+// Access statistics (utilisation table): hist[s] += sum of the kernel weights
+// of the pairs that read location s; then the fraction of locations read and
+// the KL divergence of the weighted access distribution from uniform.
+
+__global__ void __launch_bounds__(THREADS) k_access_hist(const float* __restrict__ q, Params P,
+                                                         float* __restrict__ hist) {
+  __shared__ SearchLds<WAVE> S;
+  WaveCtx c;
+  if (!wave_ctx(P, c)) return;
+  Search<NB> srch(P, S.tab, S.wave[c.wave], c.wave, c.lane);
+  WaveLds<NB>& W = S.wave[c.wave];
+  Frame* FR = S.frames[c.wave];
+  phase_a<false>(q, c.base, c.nl, P, FR, c.lane);
+  for (int t = 0; t < c.nl; ++t) {
+    const int count = srch.run(FR[t], read_sel(FR[t]), 0);
+    if (c.lane < count) unsafeAtomicAdd(hist + W.nbr[0][c.lane].slot, W.wgt[0][c.lane]);
+    wave_lds_sync();
+  }
+}
+
+__global__ void k_fill_f64(double* __restrict__ p, int n, double v) {
+  if ((int)threadIdx.x < n) p[threadIdx.x] = v;
+}
+
+__device__ __forceinline__ double wave_sum_f64(double x) {
+#pragma unroll
+  for (int mask = 1; mask < WAVE; mask <<= 1) x += __shfl_xor(x, mask);
+  return x;
+}
+
+// acc[1] += sum h log h, acc[2] += sum h, acc[3] += #{h > 0} (fp64 partials per
+// wave, one fp64 atomic per wave and sum).
+__global__ void __launch_bounds__(THREADS) k_access_reduce(const float* __restrict__ hist, int64_t N,
+                                                           double* __restrict__ acc) {
+  double hl = 0.0, hs = 0.0, hc = 0.0;
+  for (int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x; i < N; i += (int64_t)gridDim.x * THREADS) {
+    const double h = hist[i];
+    if (h > 0.0) {
+      hl += h * log(h);
+      hs += h;
+      hc += 1.0;
+    }
+  }
+  hl = wave_sum_f64(hl);
+  hs = wave_sum_f64(hs);
+  hc = wave_sum_f64(hc);
+  if (threadIdx.x % WAVE == 0) {
+    unsafeAtomicAdd(acc + 1, hl);
+    unsafeAtomicAdd(acc + 2, hs);
+    unsafeAtomicAdd(acc + 3, hc);
+  }
+}
+
+// out[0] = used fraction, out[1] = KL(p || uniform) = log N + (sum h log h)/H - log H.
+__global__ void k_access_finalize(double* __restrict__ out, int64_t N) {
+  if (threadIdx.x != 0) return;
+  const double H = out[2];
+  out[0] = out[3] / (double)N;
+  out[1] = H > 0.0 ? log((double)N) + out[1] / H - log(H) : 0.0;
+}
+
+// ---------------------------------------------------------------------------
+// Adam step (Sec. 3.2: Adam on the memory parameters) on the rows of the table
+// whose accumulated gradient row is not identically zero; the other rows keep
+// value and moments.  M lanes per row (lane = column); the gradient row is
+// cleared after use so the buffer is ready for the next accumulation.
+struct AdamArgs {
+  float lr, beta1, beta2, eps, om1, om2, bc1, bc2;  // om = 1 - beta, bc = 1 - beta^step (formed in fp64)
+};
+
+template <int DT, int M>
+__global__ void __launch_bounds__(THREADS) k_sparse_adam(void* __restrict__ table, int64_t N,
+                                                         float* __restrict__ grad, float* __restrict__ m1,
+                                                         float* __restrict__ m2, AdamArgs a) {
+  constexpr int RW = WAVE / M;  // rows per wave
+  const int lane = threadIdx.x % WAVE;
+  const int col = lane % M, sub = lane / M;
+  const uint64_t seg = (M == WAVE) ? ~0ull : (((1ull << M) - 1ull) << (M * sub));
+  const int64_t waves = (int64_t)gridDim.x * WAVES;
+  for (int64_t rb = ((int64_t)blockIdx.x * WAVES + threadIdx.x / WAVE) * RW; rb < N; rb += waves * RW) {
+    const int64_t r = rb + sub;
+    const bool in = r < N;
+    const size_t o = (size_t)(in ? r : 0) * M + col;
+    const float g = in ? grad[o] : 0.0f;
+    const bool touched = (__ballot(g != 0.0f) & seg) != 0;
+    if (in && touched) {
+      const float n1 = a.beta1 * m1[o] + a.om1 * g;
+      const float n2 = a.beta2 * m2[o] + a.om2 * (g * g);
+      m1[o] = n1;
+      m2[o] = n2;
+      const float step = a.lr * (n1 / a.bc1) / (sqrtf(n2 / a.bc2) + a.eps);
+      if constexpr (DT == LRAM_F32) {
+        float* t = reinterpret_cast<float*>(table) + o;
+        *t = *t - step;
+      } else {
+        __bf16* t = reinterpret_cast<__bf16*>(table) + o;
+        *t = (__bf16)((float)*t - step);
+      }
+      grad[o] = 0.0f;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Host side.
 
 thread_local int g_last_hip_error = 0;
@@ -2040,6 +2145,59 @@ int lram_theta_backward(const float* z, int64_t B, int64_t H, const int32_t K[8]
                         void* workspace, size_t ws_bytes, void* stream) {
   return backward_impl(z, B, H, K, table, dtype, N, m, grad_out, grad_table, grad_z, mode, workspace, ws_bytes,
                        true, (hipStream_t)stream);
+}
+
+int lram_access_histogram(const float* q, int64_t B, int64_t H, const int32_t K[8], float* hist, void* stream) {
+  int64_t L;
+  Params P;
+  int rc = check_common(q, B, H, K, &L, &P);
+  if (rc) return rc;
+  if (L == 0) return LRAM_OK;
+  if (!hist) return LRAM_EINVAL;
+  hipLaunchKernelGGL(k_access_hist, dim3(grid_for(P)), dim3(THREADS), 0, (hipStream_t)stream, q, P, hist);
+  return launched();
+}
+
+int lram_access_stats(const float* hist, int64_t N, double* out, void* stream) {
+  if (N <= 0 || !hist || !out || (reinterpret_cast<uintptr_t>(out) & 7)) return LRAM_EINVAL;
+  hipStream_t s = (hipStream_t)stream;
+  hipLaunchKernelGGL(k_fill_f64, dim3(1), dim3(WAVE), 0, s, out, 4, 0.0);
+  const int64_t blocks = (N + THREADS - 1) / THREADS;
+  hipLaunchKernelGGL(k_access_reduce, dim3((unsigned)(blocks < 4096 ? blocks : 4096)), dim3(THREADS), 0, s, hist,
+                     N, out);
+  hipLaunchKernelGGL(k_access_finalize, dim3(1), dim3(WAVE), 0, s, out, N);
+  return launched();
+}
+
+int lram_sparse_adam(void* table, int dtype, int64_t N, int32_t m, float* grad, float* exp_avg, float* exp_avg_sq,
+                     int64_t step, double lr, double beta1, double beta2, double eps, void* stream) {
+  if (dtype != LRAM_F32 && dtype != LRAM_BF16) return LRAM_EDTYPE;
+  if (m != 32 && m != 64) return LRAM_EDTYPE;
+  if (N < 0 || step < 1 || !(lr >= 0.0) || !(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0) ||
+      !(eps >= 0.0))
+    return LRAM_EINVAL;
+  if (N == 0) return LRAM_OK;
+  for (const void* ptr : {(const void*)table, (const void*)grad, (const void*)exp_avg, (const void*)exp_avg_sq})
+    if (!ptr || (reinterpret_cast<uintptr_t>(ptr) & 15)) return LRAM_EINVAL;
+  AdamArgs a;
+  a.lr = (float)lr;
+  a.beta1 = (float)beta1;
+  a.beta2 = (float)beta2;
+  a.eps = (float)eps;
+  a.om1 = (float)(1.0 - beta1);
+  a.om2 = (float)(1.0 - beta2);
+  a.bc1 = (float)(1.0 - std::pow(beta1, (double)step));
+  a.bc2 = (float)(1.0 - std::pow(beta2, (double)step));
+  const int64_t rows_per_block = (int64_t)WAVES * (WAVE / m);
+  int64_t blocks = (N + rows_per_block - 1) / rows_per_block;
+  blocks = blocks < 16384 ? blocks : 16384;
+  const dim3 g((unsigned)blocks), b(THREADS);
+  hipStream_t s = (hipStream_t)stream;
+  if (dtype == LRAM_F32 && m == 32) hipLaunchKernelGGL((k_sparse_adam<LRAM_F32, 32>), g, b, 0, s, table, N, grad, exp_avg, exp_avg_sq, a);
+  if (dtype == LRAM_F32 && m == 64) hipLaunchKernelGGL((k_sparse_adam<LRAM_F32, 64>), g, b, 0, s, table, N, grad, exp_avg, exp_avg_sq, a);
+  if (dtype == LRAM_BF16 && m == 32) hipLaunchKernelGGL((k_sparse_adam<LRAM_BF16, 32>), g, b, 0, s, table, N, grad, exp_avg, exp_avg_sq, a);
+  if (dtype == LRAM_BF16 && m == 64) hipLaunchKernelGGL((k_sparse_adam<LRAM_BF16, 64>), g, b, 0, s, table, N, grad, exp_avg, exp_avg_sq, a);
+  return launched();
 }
 
 int lram_neighbors_k(const float* q, int64_t B, int64_t H, const int32_t K[8], int32_t k, int32_t* slot, float* w,

@@ -121,6 +121,33 @@ def test_variable_k_validation(lib):
     assert lib.lram_forward_k(None, 0, 1, K4, None, 0, 4 ** 8, 32, 0, None, None) == 0
 
 
+def test_training_entry_points_validation(lib):
+    lib.lram_sparse_adam.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
+                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_double,
+                                     ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_void_p]
+    ok = dict(table=FAKE, dtype=0, N=100, m=32, grad=FAKE, m1=FAKE, m2=FAKE, step=1, lr=1e-3, b1=0.9, b2=0.999,
+              eps=1e-8)
+
+    def adam(**kw):
+        a = dict(ok, **kw)
+        return lib.lram_sparse_adam(a["table"], a["dtype"], a["N"], a["m"], a["grad"], a["m1"], a["m2"], a["step"],
+                                    a["lr"], a["b1"], a["b2"], a["eps"], None)
+
+    assert adam(step=0) == 1
+    assert adam(b1=1.0) == 1
+    assert adam(b2=-0.1) == 1
+    assert adam(lr=float("nan")) == 1
+    assert adam(m=48) == 3
+    assert adam(dtype=5) == 3
+    assert adam(grad=None) == 1
+    assert adam(m1=FAKE_MIS) == 1
+    assert adam(N=0, table=None, grad=None, m1=None, m2=None) == 0
+    assert lib.lram_access_stats(FAKE, 0, FAKE, None) == 1
+    assert lib.lram_access_stats(FAKE, 10, None, None) == 1
+    assert lib.lram_access_histogram(FAKE, 4, 1, K4, None, None) == 1
+    assert lib.lram_access_histogram(None, 0, 1, K4, None, None) == 0
+
+
 def test_auto_mode(lib):
     r = ctypes.c_int(-1)
     assert lib.lram_scatter_mode_resolved(4, 1, 3, ctypes.byref(r)) == 0 and r.value == 0        # small: atomic
