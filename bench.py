@@ -106,6 +106,23 @@ def measured_traffic(workload: str, kernel: str):
         return None
 
 
+def copy_rate(torch, dev, nbytes=1 << 30, reps=10):
+    """Attainable HBM rate: read + write bytes of a plain device-to-device copy per second."""
+    a = torch.empty(nbytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    rate = 2 * nbytes * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del a, b
+    return rate
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -286,6 +303,8 @@ def main():
         kname, kms, kbytes, kreq = "k_forward", fwd_ms, fwd_bytes, fwd_req
     achieved = kbytes / (kms * 1e-3) / 1e9
     traffic = measured_traffic(w.name, kname)
+    attainable = copy_rate(torch, dev)
+    log("attainable HBM rate (1 GiB device copy): %.0f GB/s" % attainable)
     res = {
         "metric": "lookups/sec fwd and fwd+bwd; achieved HBM GB/s vs peak (1 GPU)",
         "value": L / (ms_step * 1e-3),
@@ -310,6 +329,7 @@ def main():
         "by_k": by_k,
         "roofline": {"kernel": kname, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "attainable": attainable, "frac_attainable": achieved / attainable,
                      "bytes_per_launch": kbytes, "requested_bytes_per_launch": kreq,
                      "requested_GBps": kreq / (kms * 1e-3) / 1e9},
         "fwd_hbm_GBps": fwd_bytes / (fwd_ms * 1e-3) / 1e9,
