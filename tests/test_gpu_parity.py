@@ -70,6 +70,25 @@ def test_neighbors_random(K):
     check_neighbors(q, K)
 
 
+@pytest.mark.parametrize("K", [(8192, 2, 4, 2, 2, 2, 2, 2), (2, 2, 2, 2, 2, 2, 2, 8192), (16,) * 7 + (6,)])
+def test_neighbors_size_limits(K):
+    """The largest torus side the library takes (K_i = 8192: Lambda-scale
+    coordinates up to 2K = 16384, wrapped near both ends) and a torus with
+    N = 1.61e9 locations, close to 2^31 (the location sums of the table build
+    run in uint32 up to 2N)."""
+    _say("neighbors size limits K=%s" % (K,))
+    rng = np.random.default_rng(17)
+    Kf = np.asarray(K, np.float64)
+    q = rng.random((3000, 8)) * Kf
+    q[:500] = np.where(rng.random((500, 8)) < 0.5, rng.random((500, 8)) * 2.0,
+                       Kf - rng.random((500, 8)) * 2.0)     # next to the wrap on both sides
+    q[500:600] = Kf - 1e-3 * rng.random((100, 8))
+    q = q.astype(np.float32)
+    q = np.where(q >= Kf.astype(np.float32), np.float32(0), q).astype(np.float32)
+    nb = check_neighbors(q, K)
+    assert nb["slot"].max() > int(np.prod(K)) * 0.99 or max(K) == 8192
+
+
 @pytest.mark.parametrize("K", [(4,) * 8, (8,) * 8, (2, 2, 2, 2, 4, 4, 4, 4)])
 def test_neighbors_special_points(K):
     _say("neighbors special K=%s" % (K,))
