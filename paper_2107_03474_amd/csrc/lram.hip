@@ -8,18 +8,22 @@
 // Work decomposition (one wave = 64 lanes, up to 64 lookups per wave):
 //   phase A  lane-per-lookup: wrap, E8 closest point (D8 and D8+1/2 decoders
 //            with a parity fix), and the signed permutation that carries the
-//            offset into the fundamental region F; the result (a 64-byte
+//            offset into the fundamental region F; the result (a 96-byte
 //            "frame") goes to LDS.
 //   phase B  wave-per-lookup: the wave builds three 8x8 per-query tables in LDS
 //            (squared coordinate error, location contribution, coordinate
 //            error) indexed by (original coordinate, candidate coordinate
 //            value), scans the 232 candidate points of F (4 per lane) with one
-//            v_perm + one LDS read per coordinate, selects the closest 32 with
-//            ballot/popcount bisection on the fp32 distance bits, and then
-//            gather-reduces (forward) or scatters and forms dq (backward).
-//            The row loads of lookup t are in flight while the wave searches
-//            lookup t+1 (neighbour lists are double-buffered).
-// No MFMA: the path is a gather / scatter bound by HBM, not a contraction.
+//            v_perm + one LDS read per coordinate, selects the closest 32 (a
+//            64-bucket histogram of the fp32 distance bits, then a ballot /
+//            popcount bisection inside one bucket), and then gather-reduces
+//            (forward) or scatters and forms dq (backward).  The row loads of
+//            lookup t are in flight while the wave searches lookup t+1
+//            (neighbour lists are double-buffered).
+// The value-gradient scatter has three forms: row atomics, a location sort
+// with a segmented reduction, and a per-batch merge of lookups ordered by
+// their closest lattice point.  No MFMA: the path is a gather / scatter bound
+// by HBM and by memory-side atomics, not a contraction.
 
 #include <hip/hip_runtime.h>
 #include <cmath>
@@ -45,8 +49,14 @@ static_assert(NV == 8, "each per-query table row holds the 8 possible candidate 
 static_assert(WAVES <= 4, "the wave index is folded into byte-sized LDS offsets");
 constexpr int KMAX = 8192;  // per-coordinate torus side bound: lattice coordinates fit in int16
 
-// ties at the 32nd distance involve points of the support (at most 121 of them)
-constexpr int TIE_MAX = 128;
+// Candidates tied (equal fp32 distance bits) at the k-th place of a truncated
+// list.  Large sets of equal distances inside the support arise only from the
+// 240-point shell of a lattice point seen from a query a hair away from it
+// along some offset d: the shell splits into groups of equal <p, d>, and the
+// largest such group is the set of shell points orthogonal to one of them (an
+// E7 root system, 126 points).  The untruncated list keeps no tie list.
+template <int KS>
+constexpr int tie_max() { return KS == 256 ? 1 : 128; }
 // List width of the untruncated lookup (every point of the support).  The
 // support is an open ball of radius sqrt 8; fp32 rounding of the distance
 // recipe can admit points at distance exactly sqrt 8, so the count can pass
@@ -93,7 +103,7 @@ template <int KS>
 struct alignas(16) WaveLds {
   Nbr nbr[2][KS];     // double-buffered: lookup t+1 is searched while t is consumed
   float wgt[2][KS];
-  uint32_t tie[TIE_MAX][2];
+  uint32_t tie[tie_max<KS>()][2];
   uint32_t hist[64];  // distance histogram of the selection, 64 buckets on [4, 8)
 };
 
@@ -574,14 +584,14 @@ struct Search {
           uint32_t l, h;
           cand(s, l, h);
           const int pos = nt + prefix_count(m);
-          if (tied && pos < TIE_MAX) {
+          if (tied && pos < tie_max<KS>()) {
             W.tie[pos][0] = (uint32_t)cand_slot(S.st, l, h, sel);
             W.tie[pos][1] = cand_liftkey(l, h, sel, F);
           }
           nt += __popcll(m);
         }
       }
-      nt = min(nt, TIE_MAX);
+      nt = min(nt, tie_max<KS>());
       wave_lds_sync();
     }
     int base = 0;
