@@ -955,6 +955,11 @@ __global__ void __launch_bounds__(THREADS) k_forward_k(const float* __restrict__
   }
 }
 
+// The merged scatter pays off when lookups share their closest lattice point
+// (their neighbour lists then overlap): it is chosen when at least a tenth of
+// the lookups share theirs with another lookup of the batch.
+__device__ __forceinline__ bool merge_chosen(uint32_t shared, int64_t L) { return 10 * (int64_t)shared >= L; }
+
 // Backward, fused with the query gradient: per lookup, read the 32 rows once
 // for <G, v_j> and form dq from the coordinate errors.
 
@@ -1092,14 +1097,17 @@ __device__ __forceinline__ void grad_query(const Frame& F, const WaveLds<KS>& W,
 // atomics (EMIT = false), or emitted as (location, (lookup, w_j)) pairs for
 // the sorted segmented reduction (EMIT = true; padding gets the key N, which
 // sorts last).
+// gate (nullable): the merged scatter's device-side choice -- this kernel does
+// nothing when the batch is merged instead (see merge_chosen).
 template <int DT, int M, bool EMIT, bool TH, int KS = NB>
 __global__ void __launch_bounds__(THREADS) k_backward(const float* __restrict__ q, Params P,
                                                       const void* __restrict__ table,
                                                       const float* __restrict__ gout, float* __restrict__ gtab,
                                                       float* __restrict__ gq, uint32_t* __restrict__ pair_key,
-                                                      uint2* __restrict__ pair_val) {
+                                                      uint2* __restrict__ pair_val, const uint32_t* __restrict__ gate) {
   static_assert(!EMIT || KS == NB, "the sorted scatter takes lists of 32");
   __shared__ SearchLds<WAVE, KS> S;
+  if (gate && merge_chosen(*gate, P.L)) return;
   WaveCtx c;
   if (!wave_ctx(P, c)) return;
   const int lane = c.lane;
@@ -1424,6 +1432,23 @@ __global__ void __launch_bounds__(THREADS) k_theta_coords(const float* __restric
   if (s) s[l] = scale;
 }
 
+__global__ void k_fill_u32(uint32_t* __restrict__ p, uint32_t v) {
+  if (threadIdx.x == 0) *p = v;
+}
+
+// *count += number of positions whose sorted key equals a neighbour's.
+__global__ void __launch_bounds__(THREADS) k_count_shared(const uint32_t* __restrict__ keys, int64_t L,
+                                                          uint32_t* __restrict__ count) {
+  uint32_t c = 0;
+  for (int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x; i < L; i += (int64_t)gridDim.x * THREADS) {
+    const uint32_t k = keys[i];
+    c += ((i > 0 && keys[i - 1] == k) || (i + 1 < L && keys[i + 1] == k)) ? 1u : 0u;
+  }
+#pragma unroll
+  for (int mask = 1; mask < WAVE; mask <<= 1) c += __shfl_xor(c, mask);
+  if (threadIdx.x % WAVE == 0 && c) atomicAdd(count, c);
+}
+
 constexpr int64_t AUTO_MERGE_MIN = 131072;      // LRAM_SCATTER_AUTO merges from this many lookups on
 constexpr int MERGE_T = 64;                     // lookups per batch (one workgroup)
 constexpr int MERGE_LPW = MERGE_T / WAVES;      // lookups per wave
@@ -1478,8 +1503,10 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
                                                              const float* __restrict__ gout,
                                                              float* __restrict__ gtab, float* __restrict__ gq,
                                                              const uint32_t* __restrict__ skey,
-                                                             const uint2* __restrict__ perm) {
+                                                             const uint2* __restrict__ perm,
+                                                             const uint32_t* __restrict__ gate) {
   __shared__ FusedLds<M> S;
+  if (!merge_chosen(*gate, P.L)) return;  // the batch is scattered by k_backward instead
   const int t = threadIdx.x, wave = t / WAVE, lane = t % WAVE;
   const int64_t bbase = (int64_t)blockIdx.x * (WAVES * P.lpw);
   const int nt = (int)min<int64_t>(WAVES * P.lpw, P.L - bbase);
@@ -1851,6 +1878,7 @@ size_t sort_ws_layout(int64_t L, SortWs* ws, char* base) {
 // (lookup, 0) values, double-buffered).
 struct MergeWs {
   SortWs sort;
+  uint32_t* shared;  // lookups sharing their closest lattice point (the merge gate)
 };
 
 size_t merge_ws_layout(int64_t L, MergeWs* ws, char* base) {
@@ -1870,7 +1898,9 @@ size_t merge_ws_layout(int64_t L, MergeWs* ws, char* base) {
   char* v1 = take(n * 8);
   char* h = take(nh * 4);
   char* tt = take(nbt * 4);
+  char* sh = take(4);
   if (ws) {
+    ws->shared = (uint32_t*)sh;
     SortWs& so = ws->sort;
     so.k0 = (uint32_t*)k0; so.k1 = (uint32_t*)k1; so.v0 = (uint2*)v0; so.v1 = (uint2*)v1;
     so.hist = (uint32_t*)h; so.totals = (uint32_t*)tt;
@@ -1911,10 +1941,10 @@ struct BwdAtomicLaunch {
                 hipStream_t s) {
     if (th)
       hipLaunchKernelGGL((k_backward<DT, M, false, true>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g,
-                         gt, gq, (uint32_t*)nullptr, (uint2*)nullptr);
+                         gt, gq, (uint32_t*)nullptr, (uint2*)nullptr, (const uint32_t*)nullptr);
     else
       hipLaunchKernelGGL((k_backward<DT, M, false, false>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g,
-                         gt, gq, (uint32_t*)nullptr, (uint2*)nullptr);
+                         gt, gq, (uint32_t*)nullptr, (uint2*)nullptr, (const uint32_t*)nullptr);
     return launched();
   }
 };
@@ -1933,6 +1963,20 @@ struct BwdMergedLaunch {
     uint32_t* keys;
     uint2* perm;
     if (int rc = radix_sort(ws.sort, P.N, s, &keys, &perm)) return rc;
+    // the gate: both scatters are launched, the count decides on the device
+    // which one works (thinly spread queries have nothing to merge and keep
+    // the atomic kernel's occupancy)
+    hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(WAVE), 0, s, ws.shared, 0u);
+    const int64_t cb = (P.L + THREADS - 1) / THREADS;
+    hipLaunchKernelGGL(k_count_shared, dim3((unsigned)(cb < 2048 ? cb : 2048)), dim3(THREADS), 0, s,
+                       (const uint32_t*)keys, P.L, ws.shared);
+    if (th)
+      hipLaunchKernelGGL((k_backward<DT, M, false, true>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g,
+                         gt, gq, (uint32_t*)nullptr, (uint2*)nullptr, (const uint32_t*)ws.shared);
+    else
+      hipLaunchKernelGGL((k_backward<DT, M, false, false>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g,
+                         gt, gq, (uint32_t*)nullptr, (uint2*)nullptr, (const uint32_t*)ws.shared);
+    if (int rc = launched()) return rc;
     // one batch of at most MERGE_T lookups per workgroup
     Params Pm = P;
     Pm.lpw = P.lpw < MERGE_LPW ? P.lpw : MERGE_LPW;
@@ -1940,10 +1984,10 @@ struct BwdMergedLaunch {
     const dim3 grid((unsigned)((P.L + per_block - 1) / per_block));
     if (th)
       hipLaunchKernelGGL((k_backward_merged<DT, M, true>), grid, dim3(THREADS), 0, s, q, Pm, table, g, gt, gq,
-                         (const uint32_t*)keys, (const uint2*)perm);
+                         (const uint32_t*)keys, (const uint2*)perm, (const uint32_t*)ws.shared);
     else
       hipLaunchKernelGGL((k_backward_merged<DT, M, false>), grid, dim3(THREADS), 0, s, q, Pm, table, g, gt, gq,
-                         (const uint32_t*)keys, (const uint2*)perm);
+                         (const uint32_t*)keys, (const uint2*)perm, (const uint32_t*)ws.shared);
     return launched();
   }
 };
@@ -1954,10 +1998,10 @@ struct BwdSortedLaunch {
                 const SortWs& ws, bool th, hipStream_t s) {
     if (th)
       hipLaunchKernelGGL((k_backward<DT, M, true, true>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g,
-                         gt, gq, ws.k0, ws.v0);
+                         gt, gq, ws.k0, ws.v0, (const uint32_t*)nullptr);
     else
       hipLaunchKernelGGL((k_backward<DT, M, true, false>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g,
-                         gt, gq, ws.k0, ws.v0);
+                         gt, gq, ws.k0, ws.v0, (const uint32_t*)nullptr);
     int rc = launched();
     if (rc || !gt) return rc;
     uint32_t* kin;
@@ -2002,12 +2046,13 @@ struct BwdKLaunch {
     uint32_t* nk = nullptr;
     uint2* nv = nullptr;
     switch (width) {
-      case 16: hipLaunchKernelGGL((k_backward<DT, M, false, false, 16>), gr, b, 0, s, q, P, table, g, gt, gq, nk, nv); break;
-      case 64: hipLaunchKernelGGL((k_backward<DT, M, false, false, 64>), gr, b, 0, s, q, P, table, g, gt, gq, nk, nv); break;
+      case 16: hipLaunchKernelGGL((k_backward<DT, M, false, false, 16>), gr, b, 0, s, q, P, table, g, gt, gq, nk, nv, nullptr); break;
+      case 64: hipLaunchKernelGGL((k_backward<DT, M, false, false, 64>), gr, b, 0, s, q, P, table, g, gt, gq, nk, nv, nullptr); break;
       case KALL:
-        hipLaunchKernelGGL((k_backward<DT, M, false, false, KALL>), gr, b, 0, s, q, P, table, g, gt, gq, nk, nv);
+        hipLaunchKernelGGL((k_backward<DT, M, false, false, KALL>), gr, b, 0, s, q, P, table, g, gt, gq, nk, nv,
+                           nullptr);
         break;
-      default: hipLaunchKernelGGL((k_backward<DT, M, false, false, NB>), gr, b, 0, s, q, P, table, g, gt, gq, nk, nv); break;
+      default: hipLaunchKernelGGL((k_backward<DT, M, false, false, NB>), gr, b, 0, s, q, P, table, g, gt, gq, nk, nv, nullptr); break;
     }
     return launched();
   }
