@@ -92,14 +92,13 @@ def cpu_baseline(oracle, W, w, q_np, table, G, target_s, torch):
 def measured_traffic(workload: str, kernel: str):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 counter summary
     (FETCH_SIZE and WRITE_SIZE, copy-calibrated), or None if there is none or the
-    kernel source changed since the counters were taken."""
-    import hashlib
+    kernel sources changed since the counters were taken."""
+    from paper_2107_03474_amd.build import source_digest
 
     path = os.path.join(ROOT, "profiles", "counters_%s.json" % workload)
-    src = os.path.join(ROOT, "paper_2107_03474_amd", "csrc", "lram.hip")
     try:
         prof = json.load(open(path))
-        if prof.get("source_sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest():
+        if prof.get("source_sha256") != source_digest():
             return None
         return prof["kernels"][kernel]["traffic_bytes"]
     except (OSError, KeyError, ValueError):

@@ -1,6 +1,8 @@
 """Build liblram.so for gfx950 with hipcc (in-tree, under paper_2107_03474_amd/_build)."""
 from __future__ import annotations
 
+import glob
+import hashlib
 import os
 import subprocess
 import sys
@@ -11,7 +13,8 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(BUILD, "liblram.so")
 SOURCES = [os.path.join(CSRC, "lram.hip")]
-DEPS = SOURCES + [os.path.join(CSRC, "e8_candidates.inc"), os.path.join(ROOT, "include", "lram.h")]
+DEPS = SOURCES + sorted(glob.glob(os.path.join(CSRC, "*.h"))) + [
+    os.path.join(CSRC, "e8_candidates.inc"), os.path.join(ROOT, "include", "lram.h")]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
@@ -30,6 +33,16 @@ def hipcc() -> str:
         if c and os.path.exists(c):
             return c
     return "hipcc"
+
+
+def source_digest() -> str:
+    """sha256 over every file the library is compiled from (names and bytes, in a fixed order)."""
+    h = hashlib.sha256()
+    for d in DEPS:
+        h.update(os.path.relpath(d, ROOT).encode() + b"\0")
+        with open(d, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def build(force: bool = True, verbose: bool = False) -> str:

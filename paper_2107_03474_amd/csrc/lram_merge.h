@@ -1,0 +1,280 @@
+// lram_merge.h -- part of liblram (included by lram.hip only).
+//
+// Batch-merged scatter: closest-point keys, the activation layer's
+// coordinates, the merge gate and the fused search + per-batch merge kernel.
+
+#pragma once
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// Batch-merged scatter.  Lookups whose queries share the closest lattice point
+// share most of their 32 neighbours; the lookups are ordered by that point's
+// location (radix sort above), the backward emits (location, w) pairs in that
+// order, and each batch of MERGE_T consecutive lookups is reduced in LDS to one
+// fp32 atomic row per distinct location of the batch.
+
+// key[l] = location of the closest point of Lambda to q_l (N for a non-finite
+// query), val[l] = (l, 0).
+template <bool TH>
+__global__ void __launch_bounds__(THREADS) k_cell_key(const float* __restrict__ q, Params P,
+                                                      uint32_t* __restrict__ key, uint2* __restrict__ val) {
+  const int64_t l = (int64_t)blockIdx.x * THREADS + threadIdx.x;
+  if (l >= P.L) return;
+  float x[8], qq[8], scale;
+  int c[8];
+  load_query<TH>(q + l * in_stride<TH>(), P, qq, scale);
+  const bool valid = closest_point(qq, true, P, x, c);
+  uint32_t loc = P.N;
+  if (valid) {
+    const int eps = c[0] & 1;
+    uint32_t acc = eps ? P.N : 0u;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      int y = (c[i] - eps) >> 1;  // in [-1, K_i]
+      y = y < 0 ? y + P.K[i] : (y >= P.K[i] ? y - P.K[i] : y);
+      acc += (uint32_t)y * P.S[i];
+    }
+    loc = acc >> 1;
+  }
+  key[l] = loc;
+  val[l] = make_uint2((uint32_t)l, 0u);
+}
+
+// Activation layer coordinates: q[l] (8 fp32) and scale s[l] as the lookups see them.
+__global__ void __launch_bounds__(THREADS) k_theta_coords(const float* __restrict__ z, Params P,
+                                                          float* __restrict__ q, float* __restrict__ s) {
+  const int64_t l = (int64_t)blockIdx.x * THREADS + threadIdx.x;
+  if (l >= P.L) return;
+  float qq[8], scale;
+  load_query<true>(z + l * 16, P, qq, scale);
+  reinterpret_cast<float4*>(q + l * 8)[0] = make_float4(qq[0], qq[1], qq[2], qq[3]);
+  reinterpret_cast<float4*>(q + l * 8)[1] = make_float4(qq[4], qq[5], qq[6], qq[7]);
+  if (s) s[l] = scale;
+}
+
+__global__ void k_fill_u32(uint32_t* __restrict__ p, uint32_t v) {
+  if (threadIdx.x == 0) *p = v;
+}
+
+// *count += number of positions whose sorted key equals a neighbour's.
+__global__ void __launch_bounds__(THREADS) k_count_shared(const uint32_t* __restrict__ keys, int64_t L,
+                                                          uint32_t* __restrict__ count) {
+  uint32_t c = 0;
+  for (int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x; i < L; i += (int64_t)gridDim.x * THREADS) {
+    const uint32_t k = keys[i];
+    c += ((i > 0 && keys[i - 1] == k) || (i + 1 < L && keys[i + 1] == k)) ? 1u : 0u;
+  }
+#pragma unroll
+  for (int mask = 1; mask < WAVE; mask <<= 1) c += __shfl_xor(c, mask);
+  if (threadIdx.x % WAVE == 0 && c) atomicAdd(count, c);
+}
+
+constexpr int64_t AUTO_MERGE_MIN = 131072;      // LRAM_SCATTER_AUTO merges from this many lookups on
+constexpr int MERGE_T = 64;                     // lookups per batch (one workgroup)
+constexpr int MERGE_LPW = MERGE_T / WAVES;      // lookups per wave
+constexpr int MERGE_P = MERGE_T * NB;           // pairs per batch
+constexpr int MERGE_H = 2 * MERGE_P;            // hash entries (load factor <= 1/2)
+constexpr int MERGE_HBITS = 12;
+static_assert((1 << MERGE_HBITS) == MERGE_H, "hash size");
+constexpr int MERGE_PPT = MERGE_P / THREADS;    // pairs per thread
+constexpr int MERGE_HPT = MERGE_H / THREADS;    // hash entries per thread (consecutive)
+constexpr int32_t MERGE_EMPTY = -1;
+static_assert(MERGE_T <= 256 && MERGE_P < 65536, "batch-local indices are 8 and 16 bits wide");
+
+template <int M>
+struct alignas(16) MergeWork {
+  int32_t tag[MERGE_H];         // location of each hash entry; later pair weights and lookups in group order
+  uint32_t cnt[MERGE_H / 2];    // 16-bit pair count of each entry, then its first position in group order
+  float g[MERGE_T][M];          // upstream gradient rows of the batch
+  uint32_t wsum[WAVES][2];
+  uint32_t ngroups;
+};
+
+template <int M>
+struct alignas(16) FusedLds {
+  union {
+    struct {
+      int32_t loc[MERGE_P];     // (location, w) of every pair, [lookup in batch][j]
+      float w[MERGE_P];
+    } pairs;
+    struct {
+      int32_t loc[MERGE_P];     // distinct locations of the batch
+      uint16_t start[MERGE_P + 2];  // first position of each location's pairs in group order
+    } grp;
+  } a;
+  union {
+    SearchLds<MERGE_LPW> search;
+    MergeWork<M> merge;
+  } b;
+};
+
+// One workgroup = one batch of MERGE_T consecutive positions of the order
+// perm: each wave searches MERGE_LPW lookups (with dq as in k_backward) and
+// leaves their (location, w) pairs in LDS; then the workgroup hashes the
+// pairs by location, lays them out grouped by location, and M lanes per
+// distinct location sum w * G over its pairs and add the row with fp32 atomics.
+// Several workgroups per CU overlap one's search with another's atomics.
+// A batch in which fewer than a tenth of the lookups share their closest
+// point with a neighbour in the order (queries spread thinly over the torus)
+// has little to merge: it scatters with per-lookup atomics instead.
+template <int DT, int M, bool TH>
+__global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __restrict__ q, Params P,
+                                                             const void* __restrict__ table,
+                                                             const float* __restrict__ gout,
+                                                             float* __restrict__ gtab, float* __restrict__ gq,
+                                                             const uint32_t* __restrict__ skey,
+                                                             const uint2* __restrict__ perm,
+                                                             const uint32_t* __restrict__ gate) {
+  __shared__ FusedLds<M> S;
+  if (!merge_chosen(*gate, P.L)) return;  // the batch is scattered by k_backward instead
+  const int t = threadIdx.x, wave = t / WAVE, lane = t % WAVE;
+  const int64_t bbase = (int64_t)blockIdx.x * (WAVES * P.lpw);
+  const int nt = (int)min<int64_t>(WAVES * P.lpw, P.L - bbase);
+  bool shared = false;
+  if (t < nt) {
+    const uint32_t k = skey[bbase + t];
+    shared = (t > 0 && skey[bbase + t - 1] == k) || (t + 1 < nt && skey[bbase + t + 1] == k);
+  }
+  const bool merge = 10 * __syncthreads_count(shared) >= nt;
+  {
+    const int64_t base = bbase + (int64_t)wave * P.lpw;
+    const int nl = (int)max<int64_t>(0, min<int64_t>(P.lpw, P.L - base));
+    if (nl > 0) {
+      Search<NB> srch(P, S.b.search.tab, S.b.search.wave[wave], wave, lane);
+      WaveLds<NB>& W = S.b.search.wave[wave];
+      Frame* FR = S.b.search.frames[wave];
+      const uint32_t my_l = phase_a_perm<TH>(q, perm, base, nl, P, FR, lane);
+      const char* tb = reinterpret_cast<const char*>(table);
+      for (int i = 0; i < nl; ++i) {
+        const Frame& F = FR[i];
+        const Sel sel = read_sel(F);
+        const int count = srch.run(F, sel, 0);
+        const int64_t l = (int64_t)__builtin_amdgcn_readlane(my_l, i);
+        if (!merge && count > 0) scatter_atomic<M, NB>(W, count, gout, l, gtab, lane);
+        if (gq) grad_query<DT, M, TH, NB>(F, W, S.b.search.tab, count, tb, gout, l, lane, gq, q, P);
+        if (merge && lane < NB) {
+          const int pidx = (wave * P.lpw + i) * NB + lane;
+          S.a.pairs.loc[pidx] = W.nbr[0][lane].slot;
+          S.a.pairs.w[pidx] = W.wgt[0][lane];
+        }
+        wave_lds_sync();
+      }
+    }
+  }
+  if (!merge) return;  // uniform across the workgroup
+  __syncthreads();
+  MergeWork<M>& MW = S.b.merge;
+#pragma unroll
+  for (int k = 0; k < MERGE_HPT; ++k) MW.tag[k * THREADS + t] = MERGE_EMPTY;
+#pragma unroll
+  for (int k = 0; k < MERGE_HPT / 2; ++k) MW.cnt[k * THREADS + t] = 0u;
+  for (int i = t; i < nt * (M / 4); i += THREADS) {
+    const int r = i / (M / 4), c4 = i % (M / 4);
+    const uint32_t l = perm[bbase + r].x;
+    reinterpret_cast<float4*>(MW.g[r])[c4] = reinterpret_cast<const float4*>(gout + (size_t)l * M)[c4];
+  }
+  __syncthreads();
+  // insert every pair's location; keep (entry, rank among the entry's pairs)
+  uint32_t ent[MERGE_PPT];
+  float wv[MERGE_PPT];
+#pragma unroll
+  for (int k = 0; k < MERGE_PPT; ++k) {
+    const int pidx = k * THREADS + t;
+    ent[k] = 0xFFFFFFFFu;
+    wv[k] = 0.0f;
+    if (pidx < nt * NB) {
+      const int32_t loc = S.a.pairs.loc[pidx];
+      wv[k] = S.a.pairs.w[pidx];
+      if (loc >= 0) {
+        uint32_t h = ((uint32_t)loc * 0x9E3779B1u) >> (32 - MERGE_HBITS);
+        while (true) {
+          const int32_t old = atomicCAS(&MW.tag[h], MERGE_EMPTY, loc);
+          if (old == MERGE_EMPTY || old == loc) break;
+          h = (h + 1) & (MERGE_H - 1);
+        }
+        const uint32_t sh = 16u * (h & 1u);
+        const uint32_t rank = (atomicAdd(&MW.cnt[h >> 1], 1u << sh) >> sh) & 0xFFFFu;
+        ent[k] = h | (rank << 16);
+      }
+    }
+  }
+  __syncthreads();
+  // exclusive scan over the entries: group index and first position of each
+  // occupied entry (this thread owns entries [t*HPT, (t+1)*HPT))
+  uint32_t c[MERGE_HPT];
+  uint32_t ng = 0, np = 0;
+#pragma unroll
+  for (int k = 0; k < MERGE_HPT / 2; ++k) {
+    const uint32_t wd = MW.cnt[t * (MERGE_HPT / 2) + k];
+    c[2 * k] = wd & 0xFFFFu;
+    c[2 * k + 1] = wd >> 16;
+  }
+#pragma unroll
+  for (int k = 0; k < MERGE_HPT; ++k) {
+    ng += c[k] ? 1u : 0u;
+    np += c[k];
+  }
+  uint32_t sg = ng, sp = np;  // inclusive scan inside the wave
+#pragma unroll
+  for (int off = 1; off < WAVE; off <<= 1) {
+    const uint32_t xg = __shfl_up(sg, off), xp = __shfl_up(sp, off);
+    if (lane >= off) {
+      sg += xg;
+      sp += xp;
+    }
+  }
+  if (lane == WAVE - 1) {
+    MW.wsum[wave][0] = sg;
+    MW.wsum[wave][1] = sp;
+  }
+  __syncthreads();
+  uint32_t gb = sg - ng, pb = sp - np;
+  for (int w = 0; w < wave; ++w) {
+    gb += MW.wsum[w][0];
+    pb += MW.wsum[w][1];
+  }
+  if (t == THREADS - 1) {
+    MW.ngroups = gb + ng;
+    S.a.grp.start[gb + ng] = (uint16_t)(pb + np);
+  }
+  uint32_t first[MERGE_HPT];
+#pragma unroll
+  for (int k = 0; k < MERGE_HPT; ++k) {
+    first[k] = pb;
+    if (c[k]) {
+      S.a.grp.loc[gb] = MW.tag[t * MERGE_HPT + k];
+      S.a.grp.start[gb] = (uint16_t)pb;
+      ++gb;
+      pb += c[k];
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < MERGE_HPT / 2; ++k) MW.cnt[t * (MERGE_HPT / 2) + k] = first[2 * k] | (first[2 * k + 1] << 16);
+  __syncthreads();
+  // pairs into group order (over the dead hash tags)
+  float* pw = reinterpret_cast<float*>(MW.tag);
+  uint8_t* pt = reinterpret_cast<uint8_t*>(MW.tag + MERGE_P);
+#pragma unroll
+  for (int k = 0; k < MERGE_PPT; ++k) {
+    if (ent[k] != 0xFFFFFFFFu) {
+      const uint32_t h = ent[k] & 0xFFFFu;
+      const uint32_t pos = ((MW.cnt[h >> 1] >> (16u * (h & 1u))) & 0xFFFFu) + (ent[k] >> 16);
+      pw[pos] = wv[k];
+      pt[pos] = (uint8_t)((k * THREADS + t) / NB);
+    }
+  }
+  __syncthreads();
+  // one row per distinct location: M lanes (lane = column) sum w * G over its pairs
+  constexpr int GROUPS = THREADS / M;
+  const int col = t % M;
+  const uint32_t ngroups = MW.ngroups;
+  for (uint32_t gi = t / M; gi < ngroups; gi += GROUPS) {
+    const uint32_t p0 = S.a.grp.start[gi], p1 = S.a.grp.start[gi + 1];
+    float acc = 0.0f;
+    for (uint32_t p = p0; p < p1; ++p) acc = fmaf(pw[p], MW.g[pt[p]][col], acc);
+    unsafeAtomicAdd(gtab + (size_t)S.a.grp.loc[gi] * M + col, acc);
+  }
+}
+
+}  // namespace
