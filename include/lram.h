@@ -31,8 +31,9 @@
  *     all-padding list.
  *   - Layout.  Every tensor is dense row-major: q [L][8] fp32, table [N][m],
  *     out [L][m] (table dtype), grad_out [L][m] fp32, grad_table [N][m] fp32,
- *     grad_q [L][8] fp32, with L = B*H lookups (heads share the table,
- *     Sec. 2.3).  Device pointers must be 16-byte aligned.
+ *     grad_q [L][8] fp32, with L = B*H < 2^31 lookups (heads share the
+ *     table, Sec. 2.3).  Device pointers must be 16-byte aligned, except the
+ *     per-element outputs slot, w, d2, s and hist, which need 4 bytes.
  *   - dtype/m.  LRAM_F32 or LRAM_BF16 tables with m in {32, 64}; accumulation is
  *     always fp32.
  *   - Streams.  stream is a hipStream_t (NULL = the null stream).  All work is
@@ -60,7 +61,7 @@ extern "C" {
 
 typedef enum {
   LRAM_OK = 0,
-  LRAM_EINVAL = 1,      /* null pointer with L > 0, negative size, misaligned pointer */
+  LRAM_EINVAL = 1,      /* null pointer with L > 0, negative size, L >= 2^31, misaligned pointer */
   LRAM_EBADK = 2,       /* a K_i odd, < 2 or > 8192, N != prod K, or N >= 2^31 */
   LRAM_EDTYPE = 3,      /* unknown dtype or unsupported m for that dtype */
   LRAM_EWORKSPACE = 4,  /* workspace missing or smaller than lram_backward_workspace_bytes */

@@ -49,10 +49,16 @@ namespace {
 
 thread_local int g_last_hip_error = 0;
 
+// Alignment of the device pointers: 16 bytes where the kernels move 16-byte
+// vectors, the element size for the per-element arrays.
+bool misaligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) != 0; }
+bool misaligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3) != 0; }
+
 int check_common(const float* q, int64_t B, int64_t H, const int32_t* K, int64_t* L, Params* P) {
   if (B < 0 || H < 0 || !K) return LRAM_EINVAL;
   if (H != 0 && B > INT64_MAX / H) return LRAM_EINVAL;
   *L = B * H;
+  if (*L > LMAX) return LRAM_EINVAL;  // keeps every grid below 2^32 work-items
   int64_t N = 1;
   for (int i = 0; i < 8; ++i) {
     if (K[i] < 2 || (K[i] & 1) || K[i] > KMAX) return LRAM_EBADK;
@@ -60,7 +66,7 @@ int check_common(const float* q, int64_t B, int64_t H, const int32_t* K, int64_t
     if (N >= (int64_t(1) << 31)) return LRAM_EBADK;
   }
   if (*L > 0) {
-    if (!q || (reinterpret_cast<uintptr_t>(q) & 15)) return LRAM_EINVAL;
+    if (!q || misaligned16(q)) return LRAM_EINVAL;
   }
   for (int i = 0; i < 8; ++i) {
     P->K[i] = K[i];
@@ -84,7 +90,7 @@ int check_table(const void* table, int dtype, int64_t N, int32_t m, const Params
   if (dtype != LRAM_F32 && dtype != LRAM_BF16) return LRAM_EDTYPE;
   if (m != 32 && m != 64) return LRAM_EDTYPE;
   if (N != (int64_t)P.N) return LRAM_EBADK;
-  if (L > 0 && (!table || (reinterpret_cast<uintptr_t>(table) & 15))) return LRAM_EINVAL;
+  if (L > 0 && (!table || misaligned16(table))) return LRAM_EINVAL;
   return LRAM_OK;
 }
 
@@ -122,7 +128,7 @@ struct FwdLaunch {
   }
 };
 
-// Workspace of the sorted scatter for n = 32 L pairs (each piece 256-byte aligned).
+// Radix-sort buffers for n (key, value) pairs.
 struct SortWs {
   uint32_t *k0, *k1, *hist, *totals;
   uint2 *v0, *v1;
@@ -133,64 +139,55 @@ struct SortWs {
 
 size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
 
-size_t sort_ws_layout(int64_t L, SortWs* ws, char* base) {
-  const int64_t n = L * NB;
-  const int nblocks = (int)((n + SORT_TILE - 1) / SORT_TILE);
-  const int64_t nh = (int64_t)RADIX * nblocks;
-  const int64_t nbt = (nh + SCAN_TILE - 1) / SCAN_TILE;
+// Carves consecutive 256-byte aligned pieces out of a workspace (base = null:
+// only counts the bytes).
+struct Carver {
+  char* base;
   size_t off = 0;
-  auto take = [&](size_t bytes) {
+  char* take(size_t bytes) {
     char* ptr = base ? base + off : nullptr;
     off += align256(bytes);
     return ptr;
-  };
-  char* k0 = take(n * 4);
-  char* k1 = take(n * 4);
-  char* v0 = take(n * 8);
-  char* v1 = take(n * 8);
-  char* h = take(nh * 4);
-  char* tt = take(nbt * 4);
+  }
+};
+
+void carve_sort(int64_t n, Carver& c, SortWs* ws) {
+  const int nblocks = (int)((n + SORT_TILE - 1) / SORT_TILE);
+  const int64_t nh = (int64_t)RADIX * nblocks;
+  const int64_t nbt = (nh + SCAN_TILE - 1) / SCAN_TILE;
+  char* k0 = c.take(n * 4);
+  char* k1 = c.take(n * 4);
+  char* v0 = c.take(n * 8);
+  char* v1 = c.take(n * 8);
+  char* h = c.take(nh * 4);
+  char* tt = c.take(nbt * 4);
   if (ws) {
     ws->k0 = (uint32_t*)k0; ws->k1 = (uint32_t*)k1; ws->v0 = (uint2*)v0; ws->v1 = (uint2*)v1;
     ws->hist = (uint32_t*)h; ws->totals = (uint32_t*)tt;
     ws->n = n; ws->nblocks = nblocks; ws->nh = nh; ws->nbt = nbt;
   }
-  return off;
 }
 
-// Workspace of the batch-merged scatter for L lookups: the lookup sort (keys and
-// (lookup, 0) values, double-buffered).
+// Workspace of the sorted scatter: the sort of the 32 L (location, position) pairs.
+size_t sort_ws_layout(int64_t L, SortWs* ws, char* base) {
+  Carver c{base};
+  carve_sort(L * NB, c, ws);
+  return c.off;
+}
+
+// Workspace of the batch-merged scatter: the sort of the L lookups by the
+// location of their closest lattice point, and the merge gate's counter.
 struct MergeWs {
   SortWs sort;
   uint32_t* shared;  // lookups sharing their closest lattice point (the merge gate)
 };
 
 size_t merge_ws_layout(int64_t L, MergeWs* ws, char* base) {
-  const int64_t n = L;
-  const int nblocks = (int)((n + SORT_TILE - 1) / SORT_TILE);
-  const int64_t nh = (int64_t)RADIX * nblocks;
-  const int64_t nbt = (nh + SCAN_TILE - 1) / SCAN_TILE;
-  size_t off = 0;
-  auto take = [&](size_t bytes) {
-    char* ptr = base ? base + off : nullptr;
-    off += align256(bytes);
-    return ptr;
-  };
-  char* k0 = take(n * 4);
-  char* k1 = take(n * 4);
-  char* v0 = take(n * 8);
-  char* v1 = take(n * 8);
-  char* h = take(nh * 4);
-  char* tt = take(nbt * 4);
-  char* sh = take(4);
-  if (ws) {
-    ws->shared = (uint32_t*)sh;
-    SortWs& so = ws->sort;
-    so.k0 = (uint32_t*)k0; so.k1 = (uint32_t*)k1; so.v0 = (uint2*)v0; so.v1 = (uint2*)v1;
-    so.hist = (uint32_t*)h; so.totals = (uint32_t*)tt;
-    so.n = n; so.nblocks = nblocks; so.nh = nh; so.nbt = nbt;
-  }
-  return off;
+  Carver c{base};
+  carve_sort(L, c, ws ? &ws->sort : nullptr);
+  char* sh = c.take(4);
+  if (ws) ws->shared = (uint32_t*)sh;
+  return c.off;
 }
 
 // Stable LSD radix sort of (key, value) pairs with keys in [0, N]; returns the
@@ -351,7 +348,7 @@ int forward_impl(const float* in, int64_t B, int64_t H, const int32_t K[8], cons
   rc = check_table(table, dtype, N, m, P, L);
   if (rc) return rc;
   if (L == 0) return LRAM_OK;
-  if (!out || (reinterpret_cast<uintptr_t>(out) & 15)) return LRAM_EINVAL;
+  if (!out || misaligned16(out)) return LRAM_EINVAL;
   return dispatch<FwdLaunch>(dtype, m, in, P, table, out, th, stream);
 }
 
@@ -368,10 +365,10 @@ int backward_impl(const float* in, int64_t B, int64_t H, const int32_t K[8], con
   if (rc) return rc;
   if ((rc = resolve_mode(B, H, mode, &mode))) return rc;
   if (L == 0) return LRAM_OK;
-  if (!grad_out || (reinterpret_cast<uintptr_t>(grad_out) & 15)) return LRAM_EINVAL;
+  if (!grad_out || misaligned16(grad_out)) return LRAM_EINVAL;
   if (!grad_table && !grad_in) return LRAM_EINVAL;
-  if (grad_table && (reinterpret_cast<uintptr_t>(grad_table) & 15)) return LRAM_EINVAL;
-  if (grad_in && (reinterpret_cast<uintptr_t>(grad_in) & 15)) return LRAM_EINVAL;
+  if (grad_table && misaligned16(grad_table)) return LRAM_EINVAL;
+  if (grad_in && misaligned16(grad_in)) return LRAM_EINVAL;
   if (mode == LRAM_SCATTER_ATOMIC)
     return dispatch<BwdAtomicLaunch>(dtype, m, in, P, table, grad_out, grad_table, grad_in, th, stream);
   if (L > INT64_MAX / NB || L * NB >= (int64_t(1) << 32)) return LRAM_EINVAL;  // positions are 32-bit
@@ -424,7 +421,7 @@ int lram_neighbors(const float* q, int64_t B, int64_t H, const int32_t K[8], int
   int rc = check_common(q, B, H, K, &L, &P);
   if (rc) return rc;
   if (L == 0) return LRAM_OK;
-  if (!slot || !w) return LRAM_EINVAL;
+  if (!slot || !w || misaligned4(slot) || misaligned4(w) || misaligned4(d2)) return LRAM_EINVAL;
   hipLaunchKernelGGL(k_neighbors<NB>, dim3(grid_for(P)), dim3(THREADS), 0, (hipStream_t)stream, q, P, slot, w, d2);
   return launched();
 }
@@ -445,7 +442,7 @@ int lram_theta_coords(const float* z, int64_t B, int64_t H, const int32_t K[8], 
   int rc = check_common(z, B, H, K, &L, &P);
   if (rc) return rc;
   if (L == 0) return LRAM_OK;
-  if (!q || (reinterpret_cast<uintptr_t>(q) & 15)) return LRAM_EINVAL;
+  if (!q || misaligned16(q) || misaligned4(s)) return LRAM_EINVAL;
   hipLaunchKernelGGL(k_theta_coords, dim3((unsigned)((L + THREADS - 1) / THREADS)), dim3(THREADS), 0,
                      (hipStream_t)stream, z, P, q, s);
   return launched();
@@ -492,13 +489,13 @@ int lram_access_histogram(const float* q, int64_t B, int64_t H, const int32_t K[
   int rc = check_common(q, B, H, K, &L, &P);
   if (rc) return rc;
   if (L == 0) return LRAM_OK;
-  if (!hist) return LRAM_EINVAL;
+  if (!hist || misaligned4(hist)) return LRAM_EINVAL;
   hipLaunchKernelGGL(k_access_hist, dim3(grid_for(P)), dim3(THREADS), 0, (hipStream_t)stream, q, P, hist);
   return launched();
 }
 
 int lram_access_stats(const float* hist, int64_t N, double* out, void* stream) {
-  if (N <= 0 || !hist || !out || (reinterpret_cast<uintptr_t>(out) & 7)) return LRAM_EINVAL;
+  if (N <= 0 || !hist || !out || misaligned4(hist) || (reinterpret_cast<uintptr_t>(out) & 7)) return LRAM_EINVAL;
   hipStream_t s = (hipStream_t)stream;
   hipLaunchKernelGGL(k_fill_f64, dim3(1), dim3(WAVE), 0, s, out, 4, 0.0);
   const int64_t blocks = (N + THREADS - 1) / THREADS;
@@ -517,7 +514,7 @@ int lram_sparse_adam(void* table, int dtype, int64_t N, int32_t m, float* grad, 
     return LRAM_EINVAL;
   if (N == 0) return LRAM_OK;
   for (const void* ptr : {(const void*)table, (const void*)grad, (const void*)exp_avg, (const void*)exp_avg_sq})
-    if (!ptr || (reinterpret_cast<uintptr_t>(ptr) & 15)) return LRAM_EINVAL;
+    if (!ptr || misaligned16(ptr)) return LRAM_EINVAL;
   AdamArgs a;
   a.lr = (float)lr;
   a.beta1 = (float)beta1;
@@ -548,7 +545,7 @@ int lram_neighbors_k(const float* q, int64_t B, int64_t H, const int32_t K[8], i
   int rc = check_common(q, B, H, K, &L, &P);
   if (rc) return rc;
   if (L == 0) return LRAM_OK;
-  if (!slot || !w) return LRAM_EINVAL;
+  if (!slot || !w || misaligned4(slot) || misaligned4(w) || misaligned4(d2)) return LRAM_EINVAL;
   const dim3 g(grid_for(P)), b(THREADS);
   hipStream_t s = (hipStream_t)stream;
   switch (width) {
@@ -571,7 +568,7 @@ int lram_forward_k(const float* q, int64_t B, int64_t H, const int32_t K[8], con
   rc = check_table(table, dtype, N, m, P, L);
   if (rc) return rc;
   if (L == 0) return LRAM_OK;
-  if (!out || (reinterpret_cast<uintptr_t>(out) & 15)) return LRAM_EINVAL;
+  if (!out || misaligned16(out)) return LRAM_EINVAL;
   return dispatch<FwdKLaunch>(dtype, m, q, P, table, out, width, (hipStream_t)stream);
 }
 
@@ -587,10 +584,10 @@ int lram_backward_k(const float* q, int64_t B, int64_t H, const int32_t K[8], co
   rc = check_table(table, dtype, N, m, P, L);
   if (rc) return rc;
   if (L == 0) return LRAM_OK;
-  if (!grad_out || (reinterpret_cast<uintptr_t>(grad_out) & 15)) return LRAM_EINVAL;
+  if (!grad_out || misaligned16(grad_out)) return LRAM_EINVAL;
   if (!grad_table && !grad_q) return LRAM_EINVAL;
-  if (grad_table && (reinterpret_cast<uintptr_t>(grad_table) & 15)) return LRAM_EINVAL;
-  if (grad_q && (reinterpret_cast<uintptr_t>(grad_q) & 15)) return LRAM_EINVAL;
+  if (grad_table && misaligned16(grad_table)) return LRAM_EINVAL;
+  if (grad_q && misaligned16(grad_q)) return LRAM_EINVAL;
   return dispatch<BwdKLaunch>(dtype, m, q, P, table, grad_out, grad_table, grad_q, width, (hipStream_t)stream);
 }
 

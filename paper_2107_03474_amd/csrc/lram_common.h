@@ -19,6 +19,8 @@ constexpr int NV = E8_CAND_MAX - E8_CAND_MIN + 1;
 static_assert(NV == 8, "each per-query table row holds the 8 possible candidate coordinate values");
 static_assert(WAVES <= 4, "the wave index is folded into byte-sized LDS offsets");
 constexpr int KMAX = 8192;  // per-coordinate torus side bound: lattice coordinates fit in int16
+constexpr int XCDS = 8;  // accelerator complex dies of an MI355X
+constexpr int64_t LMAX = (int64_t(1) << 31) - 1;  // lookups per call
 
 // Candidates tied (equal fp32 distance bits) at the k-th place of a truncated
 // list.  Large sets of equal distances inside the support arise only from the
@@ -124,6 +126,15 @@ typedef float f32x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   f32x2_t v = {a, b};
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+}
+
+// Workgroup index remapped so that each XCD (the dispatcher deals consecutive
+// workgroups round-robin over the 8 XCDs, each with its own L2) walks one
+// contiguous range of the grid: a bijection on [0, gridDim.x).
+__device__ __forceinline__ int64_t xcd_block() {
+  const int64_t G = gridDim.x, b = blockIdx.x;
+  const int64_t x = b % XCDS, j = b / XCDS, q = G / XCDS, r = G % XCDS;
+  return x < r ? x * (q + 1) + j : r * (q + 1) + (x - r) * q + j;
 }
 
 }  // namespace

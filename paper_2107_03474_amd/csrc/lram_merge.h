@@ -129,7 +129,7 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
   __shared__ FusedLds<M> S;
   if (!merge_chosen(*gate, P.L)) return;  // the batch is scattered by k_backward instead
   const int t = threadIdx.x, wave = t / WAVE, lane = t % WAVE;
-  const int64_t bbase = (int64_t)blockIdx.x * (WAVES * P.lpw);
+  const int64_t bbase = xcd_block() * (WAVES * P.lpw);  // consecutive batches share an L2
   const int nt = (int)min<int64_t>(WAVES * P.lpw, P.L - bbase);
   bool shared = false;
   if (t < nt) {

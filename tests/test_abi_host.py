@@ -67,6 +67,9 @@ def test_forward_validation(lib):
     assert _fwd(lib, table=None) == 1
     assert _fwd(lib, out=None) == 1
     assert _fwd(lib, B=-1) == 1
+    assert _fwd(lib, B=1 << 31) == 1                                          # L >= 2^31 lookups
+    assert _fwd(lib, B=1 << 16, H=1 << 15) == 1
+    assert _fwd(lib, B=1 << 62, H=4) == 1                                      # B*H overflows int64
     assert _fwd(lib, q=None, table=None, out=None, B=0) == 0                  # empty: no-op
     assert _fwd(lib, q=None, table=None, out=None, H=0) == 0
 
@@ -75,6 +78,11 @@ def test_neighbors_validation(lib):
     assert lib.lram_neighbors(FAKE, 4, 1, (ctypes.c_int32 * 8)(*([5] * 8)), FAKE, FAKE, None, None) == 2
     assert lib.lram_neighbors(FAKE, 4, 1, K4, None, FAKE, None, None) == 1
     assert lib.lram_neighbors(None, 0, 7, K4, None, None, None, None) == 0
+    odd = ctypes.c_void_p(0x10002)  # not 4-byte aligned
+    assert lib.lram_neighbors(FAKE, 4, 1, K4, odd, FAKE, None, None) == 1
+    assert lib.lram_neighbors(FAKE, 4, 1, K4, FAKE, odd, None, None) == 1
+    assert lib.lram_neighbors(FAKE, 4, 1, K4, FAKE, FAKE, odd, None) == 1
+    assert lib.lram_neighbors_k(FAKE, 4, 1, K4, 16, FAKE, FAKE, odd, None) == 1
 
 
 def test_backward_validation(lib):
@@ -106,6 +114,8 @@ def test_theta_validation(lib):
     assert lib.lram_theta_forward(None, 0, 3, K4, None, 0, 4 ** 8, 32, None, None) == 0
     assert lib.lram_theta_coords(FAKE, 4, 1, K4, None, None, None) == 1
     assert lib.lram_theta_coords(None, 0, 1, K4, None, None, None) == 0
+    assert lib.lram_theta_coords(FAKE, 4, 1, K4, FAKE_MIS, None, None) == 1   # q is written as 16-byte vectors
+    assert lib.lram_theta_coords(FAKE, 4, 1, K4, FAKE, ctypes.c_void_p(0x10001), None) == 1
     assert lib.lram_theta_backward(FAKE, 4, 1, K4, FAKE, 0, 4 ** 8, 32, FAKE, None, None, 0, None, 0, None) == 1
     assert lib.lram_theta_backward(FAKE, 4, 1, K4, FAKE, 0, 4 ** 8, 32, FAKE, FAKE, FAKE, 7, None, 0, None) == 5
     assert lib.lram_theta_backward(FAKE, 4, 1, K4, FAKE, 0, 4 ** 8, 32, FAKE, FAKE, FAKE, 2, None, 0, None) == 4
@@ -146,6 +156,8 @@ def test_training_entry_points_validation(lib):
     assert lib.lram_access_stats(FAKE, 10, None, None) == 1
     assert lib.lram_access_histogram(FAKE, 4, 1, K4, None, None) == 1
     assert lib.lram_access_histogram(None, 0, 1, K4, None, None) == 0
+    assert lib.lram_access_histogram(FAKE, 4, 1, K4, ctypes.c_void_p(0x10002), None) == 1   # fp32 atomics
+    assert lib.lram_access_stats(ctypes.c_void_p(0x10002), 10, FAKE, None) == 1
 
 
 def test_auto_mode(lib):
