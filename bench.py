@@ -56,6 +56,16 @@ def unique_rows(lram, q, K, torch):
     return int(seen.numel())
 
 
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(oracle, W, w, q_np, table, G, target_s, torch):
     """The oracle on a bounded random sample of the workload's lookups (fwd+bwd)."""
     qf = q_np.reshape(-1, 8)
@@ -83,7 +93,7 @@ def cpu_baseline(oracle, W, w, q_np, table, G, target_s, torch):
             break
         n = int(min(qf.shape[0], max(2 * n, n * target_s / max(t, 1e-3))))
     cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    return {"value": n / t, "unit": "lookups/s (fwd+bwd)", "cores": cores, "kind": "oracle",
+    return {"value": n / t, "unit": "lookups/s (fwd+bwd)", "cores": cores, "kind": "oracle", "cpu": cpu_model(),
             "sample": "%d random lookups of the %s batch (%.1f s: neighbour enumeration %.1f s in C/OpenMP, "
                       "fp64 gather/grad algebra %.1f s in numpy; rows copied from the GPU table untimed)"
                       % (n, w.name, t, t_nb, t_alg)}

@@ -112,14 +112,34 @@ def _stream(t: torch.Tensor):
     return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
 
 
-def _dev(t: torch.Tensor, name: str, dtype=None):
+def _dev(t: torch.Tensor, name: str, dtype=None, shape=None, like: Optional[torch.Tensor] = None):
+    """Device pointer of t after checking what the kernels assume of it: a
+    contiguous GPU tensor (on like's device), of the given dtype and shape --
+    the C ABI takes raw pointers and cannot see a buffer's size."""
     if not t.is_cuda:
         raise LramError("%s must be a GPU tensor" % name)
+    if like is not None and t.device != like.device:
+        raise LramError("%s is on %s, expected %s" % (name, t.device, like.device))
     if not t.is_contiguous():
         raise LramError("%s must be contiguous" % name)
     if dtype is not None and t.dtype != dtype:
         raise LramError("%s must be %s" % (name, dtype))
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise LramError("%s must have shape %s, got %s" % (name, tuple(shape), tuple(t.shape)))
     return ctypes.c_void_p(t.data_ptr())
+
+
+def _table_shape(table: torch.Tensor) -> Tuple[int, int]:
+    if table.dim() != 2:
+        raise LramError("table must be [N, m]")
+    return table.shape[0], table.shape[1]
+
+
+def _workspace(ws: Optional[torch.Tensor], like: torch.Tensor):
+    """(pointer, size in bytes) of a backward workspace, (None, 0) for none."""
+    if ws is None:
+        return None, 0
+    return _dev(ws, "workspace", like=like), ws.numel() * ws.element_size()
 
 
 def _table_dtype(table: torch.Tensor) -> int:
@@ -166,15 +186,15 @@ def forward(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], out: Optiona
     """phi(q) over the closest k points (k = ALL: the whole support): [..., m] in the table dtype."""
     lib = load()
     B, H = _bh(q)
-    N, m = table.shape
+    N, m = _table_shape(table)
     if out is None:
         out = torch.empty(q.shape[:-1] + (m,), dtype=table.dtype, device=q.device)
+    args = (_dev(q, "q", torch.float32), B, H, _K(K), _dev(table, "table", like=q), _table_dtype(table), N, m)
+    o = _dev(out, "out", table.dtype, q.shape[:-1] + (m,), like=q)
     if k == NB:
-        _check(lib.lram_forward(_dev(q, "q", torch.float32), B, H, _K(K), _dev(table, "table"), _table_dtype(table),
-                                N, m, _dev(out, "out", table.dtype), _stream(q)))
+        _check(lib.lram_forward(*args, o, _stream(q)))
     else:
-        _check(lib.lram_forward_k(_dev(q, "q", torch.float32), B, H, _K(K), _dev(table, "table"),
-                                  _table_dtype(table), N, m, int(k), _dev(out, "out", table.dtype), _stream(q)))
+        _check(lib.lram_forward_k(*args, int(k), o, _stream(q)))
     return out
 
 
@@ -201,28 +221,24 @@ def backward(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], grad_out: t
     ``grad_q`` when given).  k != 32 (variable k / ALL) scatters with atomics."""
     lib = load()
     B, H = _bh(q)
-    N, m = table.shape
+    N, m = _table_shape(table)
     if grad_table is None:
         grad_table = torch.zeros((N, m), dtype=torch.float32, device=q.device)
     gq = None
     if want_grad_q:
         gq = grad_q if grad_q is not None else torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    head = (_dev(q, "q", torch.float32), B, H, _K(K), _dev(table, "table", like=q), _table_dtype(table), N, m)
+    grads = (_dev(grad_out, "grad_out", torch.float32, q.shape[:-1] + (m,), like=q),
+             _dev(grad_table, "grad_table", torch.float32, (N, m), like=q) if grad_table is not False else None,
+             _dev(gq, "grad_q", torch.float32, q.shape, like=q) if gq is not None else None)
     if k != NB:
-        gt_ptr = _dev(grad_table, "grad_table", torch.float32) if grad_table is not False else None
-        _check(lib.lram_backward_k(_dev(q, "q", torch.float32), B, H, _K(K), _dev(table, "table"),
-                                   _table_dtype(table), N, m, int(k), _dev(grad_out, "grad_out", torch.float32),
-                                   gt_ptr, _dev(gq, "grad_q") if gq is not None else None, _stream(q)))
+        _check(lib.lram_backward_k(*head, int(k), *grads, _stream(q)))
         return (grad_table if grad_table is not False else None), gq
     mode_i = _MODES[mode]
     ws_bytes = backward_workspace_bytes(B, H, m, mode_i)
     if ws_bytes and workspace is None:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
-    gt_ptr = _dev(grad_table, "grad_table", torch.float32) if grad_table is not False else None
-    _check(lib.lram_backward(_dev(q, "q", torch.float32), B, H, _K(K), _dev(table, "table"), _table_dtype(table),
-                             N, m, _dev(grad_out, "grad_out", torch.float32), gt_ptr,
-                             _dev(gq, "grad_q") if gq is not None else None, mode_i,
-                             _dev(workspace, "workspace") if workspace is not None else None,
-                             workspace.numel() if workspace is not None else 0, _stream(q)))
+    _check(lib.lram_backward(*head, *grads, mode_i, *_workspace(workspace, q), _stream(q)))
     return (grad_table if grad_table is not False else None), gq
 
 
@@ -266,11 +282,12 @@ def theta_forward(z: torch.Tensor, table: torch.Tensor, K: Sequence[int], out: O
     """theta(z) = (sum 1/|z_i|)^-1 phi((K_i / 2 pi) arg z_i): [..., m] in the table dtype."""
     lib = load()
     B, H = _bh(z, 16, "z")
-    N, m = table.shape
+    N, m = _table_shape(table)
     if out is None:
         out = torch.empty(z.shape[:-1] + (m,), dtype=table.dtype, device=z.device)
-    _check(lib.lram_theta_forward(_dev(z, "z", torch.float32), B, H, _K(K), _dev(table, "table"),
-                                  _table_dtype(table), N, m, _dev(out, "out", table.dtype), _stream(z)))
+    _check(lib.lram_theta_forward(_dev(z, "z", torch.float32), B, H, _K(K), _dev(table, "table", like=z),
+                                  _table_dtype(table), N, m, _dev(out, "out", table.dtype, z.shape[:-1] + (m,), like=z),
+                                  _stream(z)))
     return out
 
 
@@ -281,7 +298,7 @@ def theta_backward(z: torch.Tensor, table: torch.Tensor, K: Sequence[int], grad_
     (allocated zeroed if None, False to skip), grad_z [..., 16] fp32."""
     lib = load()
     B, H = _bh(z, 16, "z")
-    N, m = table.shape
+    N, m = _table_shape(table)
     if grad_table is None:
         grad_table = torch.zeros((N, m), dtype=torch.float32, device=z.device)
     gz = None
@@ -291,12 +308,12 @@ def theta_backward(z: torch.Tensor, table: torch.Tensor, K: Sequence[int], grad_
     ws_bytes = backward_workspace_bytes(B, H, m, mode_i)
     if ws_bytes and workspace is None:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=z.device)
-    gt_ptr = _dev(grad_table, "grad_table", torch.float32) if grad_table is not False else None
-    _check(lib.lram_theta_backward(_dev(z, "z", torch.float32), B, H, _K(K), _dev(table, "table"),
-                                   _table_dtype(table), N, m, _dev(grad_out, "grad_out", torch.float32), gt_ptr,
-                                   _dev(gz, "grad_z") if gz is not None else None, mode_i,
-                                   _dev(workspace, "workspace") if workspace is not None else None,
-                                   workspace.numel() if workspace is not None else 0, _stream(z)))
+    _check(lib.lram_theta_backward(
+        _dev(z, "z", torch.float32), B, H, _K(K), _dev(table, "table", like=z), _table_dtype(table), N, m,
+        _dev(grad_out, "grad_out", torch.float32, z.shape[:-1] + (m,), like=z),
+        _dev(grad_table, "grad_table", torch.float32, (N, m), like=z) if grad_table is not False else None,
+        _dev(gz, "grad_z", torch.float32, z.shape, like=z) if gz is not None else None, mode_i,
+        *_workspace(workspace, z), _stream(z)))
     return (grad_table if grad_table is not False else None), gz
 
 
@@ -333,8 +350,8 @@ def access_histogram(q: torch.Tensor, K: Sequence[int], hist: Optional[torch.Ten
     N = int(np.prod([int(k) for k in K]))
     if hist is None:
         hist = torch.zeros(N, dtype=torch.float32, device=q.device)
-    _check(lib.lram_access_histogram(_dev(q, "q", torch.float32), B, H, _K(K), _dev(hist, "hist", torch.float32),
-                                     _stream(q)))
+    _check(lib.lram_access_histogram(_dev(q, "q", torch.float32), B, H, _K(K),
+                                     _dev(hist, "hist", torch.float32, (N,), like=q), _stream(q)))
     return hist
 
 
@@ -343,6 +360,8 @@ def access_stats(hist: torch.Tensor) -> dict:
     total: summed weight, count: locations accessed} (synchronises to read them)."""
     lib = load()
     out = torch.empty(4, dtype=torch.float64, device=hist.device)
+    if hist.dim() != 1:
+        raise LramError("hist must be [N]")
     _check(lib.lram_access_stats(_dev(hist, "hist", torch.float32), hist.numel(), _dev(out, "out"), _stream(hist)))
     v = out.cpu().tolist()
     return {"used": v[0], "kl": v[1], "total": v[2], "count": int(round(v[3]))}
@@ -353,9 +372,12 @@ def sparse_adam(table: torch.Tensor, grad: torch.Tensor, exp_avg: torch.Tensor, 
     """One Adam step on the rows of ``table`` whose ``grad`` row is not all zero
     (in place; those grad rows are cleared)."""
     lib = load()
-    N, m = table.shape
-    _check(lib.lram_sparse_adam(_dev(table, "table"), _table_dtype(table), N, m, _dev(grad, "grad", torch.float32),
-                                _dev(exp_avg, "exp_avg", torch.float32), _dev(exp_avg_sq, "exp_avg_sq", torch.float32),
+    N, m = _table_shape(table)
+    f32 = torch.float32
+    _check(lib.lram_sparse_adam(_dev(table, "table"), _table_dtype(table), N, m,
+                                _dev(grad, "grad", f32, (N, m), like=table),
+                                _dev(exp_avg, "exp_avg", f32, (N, m), like=table),
+                                _dev(exp_avg_sq, "exp_avg_sq", f32, (N, m), like=table),
                                 int(step), float(lr), float(betas[0]), float(betas[1]), float(eps), _stream(table)))
 
 

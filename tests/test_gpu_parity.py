@@ -307,3 +307,36 @@ def test_workspace_errors(mode):
     small = torch.empty(need - 256, dtype=torch.uint8, device=DEV)
     with pytest.raises(lram.LramError):
         lram.backward(q, table, K, G, mode=mode, workspace=small)
+
+
+def test_binding_rejects_mismatched_buffers():
+    """The C ABI sees raw pointers only; the binding checks the shape, dtype and
+    device of every buffer before a kernel could run past its end."""
+    K = (4,) * 8
+    N = 4 ** 8
+    q = torch.rand((100, 8), device=DEV) * 4
+    z = torch.randn((100, 16), device=DEV)
+    table = _small_table(K, 32, torch.float32)
+    G = torch.randn((100, 32), device=DEV)
+    f32 = dict(dtype=torch.float32, device=DEV)
+    bad = [
+        lambda: lram.forward(q, table, K, out=torch.empty((99, 32), **f32)),
+        lambda: lram.forward(q, table, K, out=torch.empty((100, 64), **f32)),
+        lambda: lram.forward(q, table.cpu(), K),
+        lambda: lram.forward(q, table.reshape(-1), K),
+        lambda: lram.backward(q, table, K, torch.randn((100, 16), **f32)),
+        lambda: lram.backward(q, table, K, G, grad_table=torch.zeros((N - 1, 32), **f32)),
+        lambda: lram.backward(q, table, K, G, grad_q=torch.empty((100, 4), **f32)),
+        lambda: lram.backward(q, table, K, G, k=16, grad_table=torch.zeros((N, 16), **f32)),
+        lambda: lram.theta_forward(z, table, K, out=torch.empty((100, 16), **f32)),
+        lambda: lram.theta_backward(z, table, K, G, grad_z=torch.empty((100, 8), **f32)),
+        lambda: lram.access_histogram(q, K, hist=torch.zeros(N // 2, **f32)),
+        lambda: lram.access_stats(torch.zeros((N, 1), **f32)),
+        lambda: lram.sparse_adam(table, torch.zeros((N, 16), **f32), torch.zeros((N, 32), **f32),
+                                 torch.zeros((N, 32), **f32), 1),
+    ]
+    for i, call in enumerate(bad):
+        with pytest.raises(lram.LramError):
+            call()
+            pytest.fail("case %d accepted" % i)
+    torch.cuda.synchronize()
