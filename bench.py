@@ -312,6 +312,7 @@ def main():
         kname, kms, kbytes, kreq = "k_forward", fwd_ms, fwd_bytes, fwd_req
     achieved = kbytes / (kms * 1e-3) / 1e9
     traffic = measured_traffic(w.name, kname)
+    fwd_traffic = measured_traffic(w.name, "k_forward")
     attainable = copy_rate(torch, dev)
     log("attainable HBM rate (1 GiB device copy): %.0f GB/s" % attainable)
     res = {
@@ -325,7 +326,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16 table, fp32 accumulate" if w.dtype == "bf16" else "f32",
+        "dtype": "f32",  # the path's arithmetic; the table's storage type is config.table_dtype
         "data": "synthetic (seeded; see workloads.py)",
         "config": {"workload": w.name, "K": list(w.K), "locations": w.N, "m": w.m, "table_dtype": w.dtype,
                    "batch": w.B, "heads": w.H, "lookups": L, "scatter": mode, "parallelism": "none (1 GPU)"},
@@ -343,6 +344,9 @@ def main():
                      "requested_GBps": kreq / (kms * 1e-3) / 1e9},
         "fwd_hbm_GBps": fwd_bytes / (fwd_ms * 1e-3) / 1e9,
         "bwd_hbm_GBps": bwd_bytes / (bwd_ms * 1e-3) / 1e9,
+        # counter-measured HBM bytes of the forward (whole 128-byte lines for
+        # 64-byte rows) over its time; null while the counters are stale
+        "fwd_traffic_GBps": (fwd_traffic / (fwd_ms * 1e-3) / 1e9) if fwd_traffic else None,
     }
     if not args.no_cpu_baseline:
         import oracle

@@ -247,10 +247,11 @@ class LramLookup(torch.autograd.Function):
 
     @staticmethod
     def forward(ctx, q, table, K, mode):
+        q, table = q.contiguous(), table.contiguous()
         ctx.save_for_backward(q, table)
         ctx.K = tuple(int(k) for k in K)
         ctx.mode = mode
-        return forward(q.contiguous(), table.contiguous(), ctx.K)
+        return forward(q, table, ctx.K)
 
     @staticmethod
     def backward(ctx, g):
@@ -322,10 +323,11 @@ class ThetaLookup(torch.autograd.Function):
 
     @staticmethod
     def forward(ctx, z, table, K, mode):
+        z, table = z.contiguous(), table.contiguous()
         ctx.save_for_backward(z, table)
         ctx.K = tuple(int(k) for k in K)
         ctx.mode = mode
-        return theta_forward(z.contiguous(), table.contiguous(), ctx.K)
+        return theta_forward(z, table, ctx.K)
 
     @staticmethod
     def backward(ctx, g):

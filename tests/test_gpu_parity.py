@@ -340,3 +340,24 @@ def test_binding_rejects_mismatched_buffers():
             call()
             pytest.fail("case %d accepted" % i)
     torch.cuda.synchronize()
+
+
+def test_lookup_autograd_matches_abi():
+    """The autograd wrapper gives the ABI's output and gradients, also for a
+    non-contiguous query view."""
+    K = (4,) * 8
+    rng = np.random.default_rng(31)
+    q = torch.from_numpy((rng.random((8, 300)) * 4).astype(np.float32)).to(DEV).t()   # [300, 8] view
+    assert not q.is_contiguous()
+    table = _small_table(K, 32, torch.float32)
+    G = torch.randn((300, 32), device=DEV)
+    qr = q.clone().requires_grad_(True)
+    tr = table.clone().requires_grad_(True)
+    out = lram.lookup(qr, tr, K)
+    (out * G).sum().backward()
+    ref = lram.forward(q.contiguous(), table, K)
+    gt, gq = lram.backward(q.contiguous(), table, K, G)
+    torch.cuda.synchronize()
+    assert torch.equal(out.detach(), ref)
+    assert torch.equal(qr.grad, gq)
+    np.testing.assert_allclose(tr.grad.cpu().numpy(), gt.cpu().numpy(), rtol=1e-5, atol=1e-7)
