@@ -146,6 +146,7 @@ def main():
     ap.add_argument("--no-k", action="store_true", help="skip timing the variable-k lookups")
     ap.add_argument("--no-subnetwork", action="store_true", help="skip timing the memory subnetwork slice")
     ap.add_argument("--no-training", action="store_true", help="skip the access statistics and the Adam step")
+    ap.add_argument("--no-graph", action="store_true", help="skip the small-batch eager vs graph-replay timing")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (HBM counter calibration)")
     args = ap.parse_args()
@@ -360,7 +361,62 @@ def main():
         res["memory_subnetwork"] = time_subnetwork(torch, lram, log)
     if not args.no_training:
         res["training"] = time_training(torch, lram, W, log)
+    if not args.no_graph:
+        res["small_batch_graph"] = time_small_graph(torch, lram, W, log)
     print(json.dumps(res), flush=True)
+
+
+def time_small_graph(torch, lram, W, log, reps=200):
+    """The 4,096-lookup configurations are launch-bound: one forward + backward
+    step launched eagerly through the binding, and the same step captured once
+    into a HIP graph and replayed (microseconds per step, `reps` steps back to
+    back; the gradient table accumulates across steps)."""
+    out = {}
+    for name in ("k4-m32-f32-uniform", "k4-m32-f32-gmm64"):
+        w = W.WORKLOADS[name]
+        q = torch.from_numpy(W.queries(w)).to("cuda")
+        table = W.make_table(w, torch.device("cuda"))
+        G = W.grad_out(w, torch.device("cuda"))
+        gtab = torch.zeros((w.N, w.m), dtype=torch.float32, device="cuda")
+        o = torch.empty((w.B, w.H, w.m), dtype=table.dtype, device="cuda")
+        gq = torch.empty((w.B, w.H, 8), dtype=torch.float32, device="cuda")
+        mode = lram.resolved_mode(w.B, w.H, "auto")
+        nws = lram.backward_workspace_bytes(w.B, w.H, w.m, mode)
+        ws = torch.empty(nws, dtype=torch.uint8, device="cuda") if nws else None
+
+        def step():
+            lram.forward(q, table, w.K, out=o)
+            lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, mode=mode, workspace=ws)
+
+        def timed(f):
+            for _ in range(10):
+                f()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                f()
+            e1.record()
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / reps * 1e3
+
+        eager_us = timed(step)
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        graph_us = timed(graph.replay)
+        out[name] = {"lookups": w.L, "scatter": mode, "eager_us": eager_us, "graph_us": graph_us,
+                     "graph_lookups_per_s": w.L / (graph_us * 1e-6)}
+        log("%s: fwd+bwd step %.1f us eager, %.1f us graph replay" % (name, eager_us, graph_us))
+        del graph, q, table, G, gtab, o, gq, ws
+        torch.cuda.empty_cache()
+    return out
 
 
 def time_training(torch, lram, W, log, batches=16):
