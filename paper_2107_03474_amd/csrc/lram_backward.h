@@ -69,47 +69,47 @@ __device__ __forceinline__ void grad_query(const Frame& F, const WaveLds<KS>& W,
       lsel[k] = F.sel[(ch + k * G::LPR) & 7];
     }
     for (int r0 = 0; r0 < (KS == NB ? 1 : count); r0 += R) {
-    uint4 v[G::NP];
-    int32_t sl[G::NP];
+      uint4 v[G::NP];
+      int32_t sl[G::NP];
 #pragma unroll
-    for (int p = 0; p < G::NP; ++p) {
-      sl[p] = W.nbr[0][r0 + p * G::RPP + rsub].slot;
-      v[p] = sl[p] >= 0 ? *reinterpret_cast<const uint4*>(tb + (size_t)sl[p] * G::RB + ch * 16)
-                        : make_uint4(0, 0, 0, 0);
-    }
+      for (int p = 0; p < G::NP; ++p) {
+        sl[p] = W.nbr[0][r0 + p * G::RPP + rsub].slot;
+        v[p] = sl[p] >= 0 ? *reinterpret_cast<const uint4*>(tb + (size_t)sl[p] * G::RB + ch * 16)
+                          : make_uint4(0, 0, 0, 0);
+      }
 #pragma unroll
-    for (int p = 0; p < G::NP; ++p) {
-      const int j = r0 + p * G::RPP + rsub;
-      float f[G::EPC];
-      unpack16<DT, G::EPC>(v[p], f);
-      // <G, v_j>: this lane's chunk, then a sum over the LPR lanes of the row,
-      // in fp64 (fp32 x fp32 products are exact there).  Next to a lattice
-      // point one term carries all of dq (and behind the activation layer
-      // dL/ds is sum_j w_j <G, v_j>), so a cancelling fp32 dot product would
-      // become the relative error of the whole gradient.
-      double pd64 = 0.0;
+      for (int p = 0; p < G::NP; ++p) {
+        const int j = r0 + p * G::RPP + rsub;
+        float f[G::EPC];
+        unpack16<DT, G::EPC>(v[p], f);
+        // <G, v_j>: this lane's chunk, then a sum over the LPR lanes of the row,
+        // in fp64 (fp32 x fp32 products are exact there).  Next to a lattice
+        // point one term carries all of dq (and behind the activation layer
+        // dL/ds is sum_j w_j <G, v_j>), so a cancelling fp32 dot product would
+        // become the relative error of the whole gradient.
+        double pd64 = 0.0;
 #pragma unroll
-      for (int e = 0; e < G::EPC; ++e) pd64 = fma((double)g[e], (double)f[e], pd64);
+        for (int e = 0; e < G::EPC; ++e) pd64 = fma((double)g[e], (double)f[e], pd64);
 #pragma unroll
-      for (int mask = 1; mask < G::LPR; mask <<= 1) pd64 += __shfl_xor(pd64, mask);
-      if (sl[p] >= 0) {
-        const Nbr n = W.nbr[0][j];
-        const float u = 1.0f - __uint_as_float(n.dbits) * 0.125f;
-        const double a = -2.0 * (double)(u * u * u) * pd64;
-        if constexpr (TH) {
-          const float u2 = u * u;
-          dls = fma((double)(u2 * u2), pd64, dls);
-        }
+        for (int mask = 1; mask < G::LPR; mask <<= 1) pd64 += __shfl_xor(pd64, mask);
+        if (sl[p] >= 0) {
+          const Nbr n = W.nbr[0][j];
+          const float u = 1.0f - __uint_as_float(n.dbits) * 0.125f;
+          const double a = -2.0 * (double)(u * u * u) * pd64;
+          if constexpr (TH) {
+            const float u2 = u * u;
+            dls = fma((double)(u2 * u2), pd64, dls);
+          }
 #pragma unroll
-        for (int k = 0; k < ICOORD; ++k) {
-          const int i = ch + k * G::LPR;
-          if (i < 8) {
-            const uint32_t ab = __builtin_amdgcn_perm(n.hi, n.lo, lsel[k]);
-            dq[k] = fma(a, (double)lds_f32(T.et, ab + 256u * i), dq[k]);
+          for (int k = 0; k < ICOORD; ++k) {
+            const int i = ch + k * G::LPR;
+            if (i < 8) {
+              const uint32_t ab = __builtin_amdgcn_perm(n.hi, n.lo, lsel[k]);
+              dq[k] = fma(a, (double)lds_f32(T.et, ab + 256u * i), dq[k]);
+            }
           }
         }
       }
-    }
     }  // chunks of R rows
   }
 #pragma unroll
