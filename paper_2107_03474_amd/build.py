@@ -4,6 +4,7 @@ from __future__ import annotations
 import glob
 import hashlib
 import os
+import re
 import subprocess
 import sys
 
@@ -35,13 +36,23 @@ def hipcc() -> str:
     return "hipcc"
 
 
+def _code_text(path: str) -> bytes:
+    """A source file with its comments dropped and whitespace collapsed: edits
+    that cannot change the compiled code leave it unchanged."""
+    with open(path, encoding="utf-8") as f:
+        txt = f.read()
+    txt = re.sub(r"/\*.*?\*/", " ", txt, flags=re.S)
+    txt = re.sub(r"//[^\n]*", " ", txt)
+    return " ".join(txt.split()).encode()
+
+
 def source_digest() -> str:
-    """sha256 over every file the library is compiled from (names and bytes, in a fixed order)."""
+    """sha256 over the code of every file the library is compiled from (names
+    and comment-free text, in a fixed order)."""
     h = hashlib.sha256()
     for d in DEPS:
         h.update(os.path.relpath(d, ROOT).encode() + b"\0")
-        with open(d, "rb") as f:
-            h.update(f.read())
+        h.update(_code_text(d) + b"\0")
     return h.hexdigest()
 
 
