@@ -151,8 +151,8 @@ def main():
                     help="only run a plain 1 GiB device-to-device copy 5 times (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path (each GPU would run the "
-              "same kernels on its own shard of the table; see DESIGN.md). Use --gpus 1.", file=sys.stderr)
+        print("bench.py runs on one GPU only: there is no multi-GPU path (each GPU would run the same "
+              "kernels on its own shard of the table). Use --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -221,6 +221,15 @@ def main():
     bwd_ms = float(np.mean([ev[k][1].elapsed_time(ev[k][2]) for k in range(args.steps)]))
     ms_step = wall * 1e3 / args.steps
     log("timed %d steps: %.3f ms/step (forward %.3f ms, backward %.3f ms)" % (args.steps, ms_step, fwd_ms, bwd_ms))
+    # what the accumulate-into contract spares every step: clearing the whole
+    # gradient table (outside the timed steps, not part of `value`)
+    ez = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ez[0].record()
+    gtab.zero_()
+    ez[1].record()
+    torch.cuda.synchronize()
+    zero_ms = ez[0].elapsed_time(ez[1])
+    log("clearing the %.1f GB gradient table: %.2f ms" % (gtab.numel() * 4 / 1e9, zero_ms))
 
     # the other value-gradient scatters, timed the same way for comparison (not part of `value`)
     by_scatter = {mode: bwd_ms}
@@ -336,6 +345,7 @@ def main():
         "bwd_ms": bwd_ms,
         "bwd_ms_by_scatter": by_scatter,
         "distinct_rows": U,
+        "grad_table_zero_ms": zero_ms,
         "theta": theta,
         "by_k": by_k,
         "roofline": {"kernel": kname, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -345,6 +355,9 @@ def main():
                      "requested_GBps": kreq / (kms * 1e-3) / 1e9},
         "fwd_hbm_GBps": fwd_bytes / (fwd_ms * 1e-3) / 1e9,
         "bwd_hbm_GBps": bwd_bytes / (bwd_ms * 1e-3) / 1e9,
+        # requested bytes (every lookup reads its 32 rows) over time
+        "fwd_requested_GBps": fwd_req / (fwd_ms * 1e-3) / 1e9,
+        "bwd_requested_GBps": bwd_req / (bwd_ms * 1e-3) / 1e9,
         # counter-measured HBM bytes of the forward (whole 128-byte lines for
         # 64-byte rows) over its time; null while the counters are stale
         "fwd_traffic_GBps": (fwd_traffic / (fwd_ms * 1e-3) / 1e9) if fwd_traffic else None,
