@@ -12,7 +12,9 @@ Lattices"):
   within the kernel support r^2 < 8 (Sec. 2.5, Sec. 2.6), enumerated straight
   from the definition by the C helper ``lram_oracle.c``; their locations on the
   torus (Sec. 2.2), the fp32 recipe distances that decide the selection and
-  the kernel weights f(r) = (1 - r^2/8)^4 in fp64.
+  the kernel weights f(r) = (1 - r^2/8)^4 in fp64.  ``k`` = 16 or 64 keeps
+  that many instead, ``k`` = 0 every point of the support (the untruncated
+  sum of Sec. 2.2 / 2.5).
 * ``forward``    -- phi_32(q) = sum_j w_j v_{slot_j} (Sec. 2.2 with the
   truncation of Sec. 2.6), accumulated in fp64.
 * ``backward``   -- the gradients of <G, phi_32(q)> with respect to the value
@@ -25,6 +27,12 @@ Lattices"):
   theta(z) = (sum_i 1/|z_i|)^-1 phi_32((K_i / 2 pi) arg z_i) for z in C^8,
   given as 16 reals (Re z_0, Im z_0, ..., Re z_7, Im z_7), and its gradients
   with respect to z (through arg and the scale) and to the value table.
+* ``sparse_adam`` -- one Adam step (Sec. 3.2 trains the memory with Adam at
+  learning rate 1e-3) applied only to the rows whose gradient is not all zero.
+* ``access_histogram``, ``access_stats`` -- the weighted access count of every
+  location and, from it, the share of locations used and the KL divergence
+  of the access distribution from uniform (the statistics of Sec. 4.3).
+* ``oracle.subnetwork`` -- the memory subnetwork of Sec. 3.1 around theta.
 
 Scale and the other readings of the paper are stated in the header of
 ``lram_oracle.c``.  All functions take numpy arrays on the host.
