@@ -286,10 +286,13 @@ def main():
         by_k = {}
         qs = q.reshape(-1, 8)[:65536]
         tot_all = lram.neighbors(qs, w.K, want_d2=False, k=lram.ALL)[1].double().sum(1)
+        nws = lram.backward_workspace_bytes(w.B, w.H, w.m, "merged")
+        wsm = torch.empty(nws, dtype=torch.uint8, device=dev)
         for kk in (16, 32, 64, lram.ALL):
-            e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
             lram.forward(q, table, w.K, out=out, k=kk)
             lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, k=kk, mode="atomic")
+            lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, k=kk, mode="merged", workspace=wsm)
             torch.cuda.synchronize()
             e[0].record(stream)
             for _ in range(3):
@@ -298,13 +301,17 @@ def main():
             for _ in range(3):
                 lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, k=kk, mode="atomic")
             e[2].record(stream)
+            for _ in range(3):
+                lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, k=kk, mode="merged", workspace=wsm)
+            e[3].record(stream)
             torch.cuda.synchronize()
             cov = (lram.neighbors(qs, w.K, want_d2=False, k=kk)[1].double().sum(1) / tot_all).mean().item()
             name = "all" if kk == lram.ALL else str(kk)
             by_k[name] = {"fwd_ms": e[0].elapsed_time(e[1]) / 3, "bwd_atomic_ms": e[1].elapsed_time(e[2]) / 3,
-                          "coverage": cov}
-            log("k=%s: forward %.3f ms, backward (atomic) %.3f ms, weight coverage %.6f" % (
-                name, by_k[name]["fwd_ms"], by_k[name]["bwd_atomic_ms"], cov))
+                          "bwd_merged_ms": e[2].elapsed_time(e[3]) / 3, "coverage": cov}
+            log("k=%s: forward %.3f ms, backward %.3f ms atomic / %.3f ms merged, weight coverage %.6f" % (
+                name, by_k[name]["fwd_ms"], by_k[name]["bwd_atomic_ms"], by_k[name]["bwd_merged_ms"], cov))
+        del wsm
 
     st = 4 if w.dtype == "f32" else 2
     L = w.L

@@ -65,7 +65,7 @@ typedef enum {
   LRAM_EBADK = 2,       /* a K_i odd, < 2 or > 8192, N != prod K, or N >= 2^31 */
   LRAM_EDTYPE = 3,      /* unknown dtype or unsupported m for that dtype */
   LRAM_EWORKSPACE = 4,  /* workspace missing or smaller than lram_backward_workspace_bytes */
-  LRAM_EMODE = 5,       /* unknown scatter mode */
+  LRAM_EMODE = 5,       /* unknown scatter mode, or the sorted mode with k != 32 */
   LRAM_EHIP = 6         /* a HIP launch failed; see lram_last_hip_error */
 } lram_status;
 
@@ -112,7 +112,8 @@ int lram_forward(const float* q, int64_t B, int64_t H, const int32_t K[8], const
 
 /*
  * lram_backward_workspace_bytes -- device workspace needed by lram_backward
- * for L = B*H lookups in the given scatter mode (0 for LRAM_SCATTER_ATOMIC).
+ * (and lram_backward_k, lram_theta_backward) for L = B*H lookups in the given
+ * scatter mode (0 for LRAM_SCATTER_ATOMIC; the same for every k).
  */
 int lram_backward_workspace_bytes(int64_t B, int64_t H, int32_t m, int mode, size_t* bytes);
 
@@ -136,8 +137,8 @@ int lram_scatter_mode_resolved(int64_t B, int64_t H, int mode, int* resolved);
  * The neighbour search is recomputed from q.  workspace/ws_bytes: device
  * buffer, 256-byte aligned, of at least lram_backward_workspace_bytes (may be
  * NULL for the atomic mode); its contents on entry do not matter.  The sorted
- * and merged modes need 32 L < 2^32.  grad_table may be NULL only if grad_q is
- * not (without grad_table every mode computes grad_q the same way).
+ * mode needs 32 L < 2^32.  grad_table may be NULL only if grad_q is not
+ * (without grad_table every mode computes grad_q the same way).
  */
 int lram_backward(const float* q, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
                   int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_q, int mode,
@@ -182,8 +183,8 @@ int lram_sparse_adam(void* table, int dtype, int64_t N, int32_t m, float* grad, 
  * arithmetic (Table 1); the recipe's rounding can admit points at distance
  * exactly sqrt 8, but never more than the 1 + 240 that a ball of that radius
  * holds, so LRAM_ALL lists are LRAM_MAX_SUPPORT wide.  Lists are padded with
- * slot -1, weight 0.  The backward scatters with fp32 atomics (the sorted and
- * merged scatters take k = 32 only) and needs no workspace.
+ * slot -1, weight 0.  The backward takes the atomic and merged scatters (and
+ * LRAM_SCATTER_AUTO); the sorted scatter takes k = 32 only (LRAM_EMODE).
  */
 
 /* lram_neighbors_k -- as lram_neighbors with lists of width w = k (LRAM_MAX_SUPPORT
@@ -195,10 +196,12 @@ int lram_neighbors_k(const float* q, int64_t B, int64_t H, const int32_t K[8], i
 int lram_forward_k(const float* q, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
                    int64_t N, int32_t m, int32_t k, void* out, void* stream);
 
-/* lram_backward_k -- lram_backward's gradients for the k-point lookup (atomic scatter). */
+/* lram_backward_k -- lram_backward's gradients for the k-point lookup; mode,
+ * workspace and ws_bytes as for lram_backward (the merged scatter merges the
+ * k pairs of every lookup; a batch holds 64 lookups for k <= 32, 2048/k above). */
 int lram_backward_k(const float* q, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
                     int64_t N, int32_t m, int32_t k, const float* grad_out, float* grad_table, float* grad_q,
-                    void* stream);
+                    int mode, void* workspace, size_t ws_bytes, void* stream);
 
 /*
  * Activation layer in front of the lookup (Sec. 2.3).  Each lookup takes 8

@@ -73,7 +73,8 @@ def load():
             lib.lram_neighbors_k.restype = I
             lib.lram_forward_k.argtypes = [P, I64, I64, P, P, I, I64, I32, I32, P, P]
             lib.lram_forward_k.restype = I
-            lib.lram_backward_k.argtypes = [P, I64, I64, P, P, I, I64, I32, I32, P, P, P, P]
+            lib.lram_backward_k.argtypes = [P, I64, I64, P, P, I, I64, I32, I32, P, P, P, I, P, ctypes.c_size_t,
+                                            P]
             lib.lram_backward_k.restype = I
             lib.lram_access_histogram.argtypes = [P, I64, I64, P, P, P]
             lib.lram_access_histogram.restype = I
@@ -218,7 +219,8 @@ def backward(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], grad_out: t
              workspace: Optional[torch.Tensor] = None, grad_q: Optional[torch.Tensor] = None, k: int = NB):
     """Gradients: grad_table [N, m] fp32 is ACCUMULATED into (allocated zeroed if None,
     pass False to skip), grad_q [..., 8] fp32 (None unless want_grad_q; written into
-    ``grad_q`` when given).  k != 32 (variable k / ALL) scatters with atomics."""
+    ``grad_q`` when given).  k != 32 (variable k / ALL) takes the atomic and
+    merged scatters (and "auto"), not the sorted one."""
     lib = load()
     B, H = _bh(q)
     N, m = _table_shape(table)
@@ -231,14 +233,14 @@ def backward(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], grad_out: t
     grads = (_dev(grad_out, "grad_out", torch.float32, q.shape[:-1] + (m,), like=q),
              _dev(grad_table, "grad_table", torch.float32, (N, m), like=q) if grad_table is not False else None,
              _dev(gq, "grad_q", torch.float32, q.shape, like=q) if gq is not None else None)
-    if k != NB:
-        _check(lib.lram_backward_k(*head, int(k), *grads, _stream(q)))
-        return (grad_table if grad_table is not False else None), gq
     mode_i = _MODES[mode]
     ws_bytes = backward_workspace_bytes(B, H, m, mode_i)
     if ws_bytes and workspace is None:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
-    _check(lib.lram_backward(*head, *grads, mode_i, *_workspace(workspace, q), _stream(q)))
+    if k != NB:
+        _check(lib.lram_backward_k(*head, int(k), *grads, mode_i, *_workspace(workspace, q), _stream(q)))
+    else:
+        _check(lib.lram_backward(*head, *grads, mode_i, *_workspace(workspace, q), _stream(q)))
     return (grad_table if grad_table is not False else None), gq
 
 

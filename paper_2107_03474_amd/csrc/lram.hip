@@ -215,17 +215,64 @@ int radix_sort(const SortWs& ws, uint32_t N, hipStream_t s, uint32_t** kres, uin
   return LRAM_OK;
 }
 
-// q is the lookups' input: q [L][8], or z [L][16] when th (activation layer).
+// q is the lookups' input: q [L][8], or z [L][16] when TH (activation layer).
+// The atomic backward kernel for lists of KS; gate is the merged scatter's
+// device-side choice (null: always scatter).
+template <int DT, int M, bool TH, int KS>
+void launch_atomic(const float* q, const Params& P, const void* table, const float* g, float* gt, float* gq,
+                   const uint32_t* gate, hipStream_t s) {
+  hipLaunchKernelGGL((k_backward<DT, M, false, TH, KS>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g,
+                     gt, gq, (uint32_t*)nullptr, (uint2*)nullptr, gate);
+}
+
+// The merged scatter for lists of KS: cell keys, the lookup sort and the
+// gate's count, then both the atomic kernel and the merged kernel -- the count
+// decides on the device which one works (thinly spread queries have nothing
+// to merge and keep the atomic kernel's occupancy).
+template <int DT, int M, bool TH, int KS>
+int merged_pass(const float* q, const Params& P, const void* table, const float* g, float* gt, float* gq,
+                const MergeWs& ws, hipStream_t s) {
+  if (!gt) {
+    launch_atomic<DT, M, TH, KS>(q, P, table, g, gt, gq, nullptr, s);
+    return launched();
+  }
+  const dim3 kgrid((unsigned)((P.L + THREADS - 1) / THREADS));
+  hipLaunchKernelGGL(k_cell_key<TH>, kgrid, dim3(THREADS), 0, s, q, P, ws.sort.k0, ws.sort.v0);
+  if (int rc = launched()) return rc;
+  uint32_t* keys;
+  uint2* perm;
+  if (int rc = radix_sort(ws.sort, P.N, s, &keys, &perm)) return rc;
+  hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(WAVE), 0, s, ws.shared, 0u);
+  const int64_t cb = (P.L + THREADS - 1) / THREADS;
+  hipLaunchKernelGGL(k_count_shared, dim3((unsigned)(cb < 2048 ? cb : 2048)), dim3(THREADS), 0, s,
+                     (const uint32_t*)keys, P.L, ws.shared);
+  launch_atomic<DT, M, TH, KS>(q, P, table, g, gt, gq, ws.shared, s);
+  if (int rc = launched()) return rc;
+  // one batch of at most merge_t<KS>() lookups per workgroup
+  Params Pm = P;
+  Pm.lpw = P.lpw < merge_lpw<KS>() ? P.lpw : merge_lpw<KS>();
+  const int64_t per_block = (int64_t)Pm.lpw * WAVES;
+  const dim3 grid((unsigned)((P.L + per_block - 1) / per_block));
+  hipLaunchKernelGGL((k_backward_merged<DT, M, TH, KS>), grid, dim3(THREADS), 0, s, q, Pm, table, g, gt, gq,
+                     (const uint32_t*)keys, (const uint2*)perm, (const uint32_t*)ws.shared);
+  return launched();
+}
+
+// width: list width (16, 32, 64 or KALL); th: the activation layer (width 32 only).
 template <int DT, int M>
 struct BwdAtomicLaunch {
   static int go(const float* q, const Params& P, const void* table, const float* g, float* gt, float* gq, bool th,
-                hipStream_t s) {
-    if (th)
-      hipLaunchKernelGGL((k_backward<DT, M, false, true>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g,
-                         gt, gq, (uint32_t*)nullptr, (uint2*)nullptr, (const uint32_t*)nullptr);
-    else
-      hipLaunchKernelGGL((k_backward<DT, M, false, false>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g,
-                         gt, gq, (uint32_t*)nullptr, (uint2*)nullptr, (const uint32_t*)nullptr);
+                int width, hipStream_t s) {
+    if (th) {
+      launch_atomic<DT, M, true, NB>(q, P, table, g, gt, gq, nullptr, s);
+    } else {
+      switch (width) {
+        case 16: launch_atomic<DT, M, false, 16>(q, P, table, g, gt, gq, nullptr, s); break;
+        case 64: launch_atomic<DT, M, false, 64>(q, P, table, g, gt, gq, nullptr, s); break;
+        case KALL: launch_atomic<DT, M, false, KALL>(q, P, table, g, gt, gq, nullptr, s); break;
+        default: launch_atomic<DT, M, false, NB>(q, P, table, g, gt, gq, nullptr, s); break;
+      }
+    }
     return launched();
   }
 };
@@ -233,43 +280,14 @@ struct BwdAtomicLaunch {
 template <int DT, int M>
 struct BwdMergedLaunch {
   static int go(const float* q, const Params& P, const void* table, const float* g, float* gt, float* gq,
-                const MergeWs& ws, bool th, hipStream_t s) {
-    if (!gt) return BwdAtomicLaunch<DT, M>::go(q, P, table, g, gt, gq, th, s);
-    const dim3 kgrid((unsigned)((P.L + THREADS - 1) / THREADS));
-    if (th)
-      hipLaunchKernelGGL(k_cell_key<true>, kgrid, dim3(THREADS), 0, s, q, P, ws.sort.k0, ws.sort.v0);
-    else
-      hipLaunchKernelGGL(k_cell_key<false>, kgrid, dim3(THREADS), 0, s, q, P, ws.sort.k0, ws.sort.v0);
-    if (int rc = launched()) return rc;
-    uint32_t* keys;
-    uint2* perm;
-    if (int rc = radix_sort(ws.sort, P.N, s, &keys, &perm)) return rc;
-    // the gate: both scatters are launched, the count decides on the device
-    // which one works (thinly spread queries have nothing to merge and keep
-    // the atomic kernel's occupancy)
-    hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(WAVE), 0, s, ws.shared, 0u);
-    const int64_t cb = (P.L + THREADS - 1) / THREADS;
-    hipLaunchKernelGGL(k_count_shared, dim3((unsigned)(cb < 2048 ? cb : 2048)), dim3(THREADS), 0, s,
-                       (const uint32_t*)keys, P.L, ws.shared);
-    if (th)
-      hipLaunchKernelGGL((k_backward<DT, M, false, true>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g,
-                         gt, gq, (uint32_t*)nullptr, (uint2*)nullptr, (const uint32_t*)ws.shared);
-    else
-      hipLaunchKernelGGL((k_backward<DT, M, false, false>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g,
-                         gt, gq, (uint32_t*)nullptr, (uint2*)nullptr, (const uint32_t*)ws.shared);
-    if (int rc = launched()) return rc;
-    // one batch of at most MERGE_T lookups per workgroup
-    Params Pm = P;
-    Pm.lpw = P.lpw < MERGE_LPW ? P.lpw : MERGE_LPW;
-    const int64_t per_block = (int64_t)Pm.lpw * WAVES;
-    const dim3 grid((unsigned)((P.L + per_block - 1) / per_block));
-    if (th)
-      hipLaunchKernelGGL((k_backward_merged<DT, M, true>), grid, dim3(THREADS), 0, s, q, Pm, table, g, gt, gq,
-                         (const uint32_t*)keys, (const uint2*)perm, (const uint32_t*)ws.shared);
-    else
-      hipLaunchKernelGGL((k_backward_merged<DT, M, false>), grid, dim3(THREADS), 0, s, q, Pm, table, g, gt, gq,
-                         (const uint32_t*)keys, (const uint2*)perm, (const uint32_t*)ws.shared);
-    return launched();
+                const MergeWs& ws, bool th, int width, hipStream_t s) {
+    if (th) return merged_pass<DT, M, true, NB>(q, P, table, g, gt, gq, ws, s);
+    switch (width) {
+      case 16: return merged_pass<DT, M, false, 16>(q, P, table, g, gt, gq, ws, s);
+      case 64: return merged_pass<DT, M, false, 64>(q, P, table, g, gt, gq, ws, s);
+      case KALL: return merged_pass<DT, M, false, KALL>(q, P, table, g, gt, gq, ws, s);
+      default: return merged_pass<DT, M, false, NB>(q, P, table, g, gt, gq, ws, s);
+    }
   }
 };
 
@@ -319,26 +337,6 @@ struct FwdKLaunch {
   }
 };
 
-template <int DT, int M>
-struct BwdKLaunch {
-  static int go(const float* q, const Params& P, const void* table, const float* g, float* gt, float* gq, int width,
-                hipStream_t s) {
-    const dim3 gr(grid_for(P)), b(THREADS);
-    uint32_t* nk = nullptr;
-    uint2* nv = nullptr;
-    switch (width) {
-      case 16: hipLaunchKernelGGL((k_backward<DT, M, false, false, 16>), gr, b, 0, s, q, P, table, g, gt, gq, nk, nv, nullptr); break;
-      case 64: hipLaunchKernelGGL((k_backward<DT, M, false, false, 64>), gr, b, 0, s, q, P, table, g, gt, gq, nk, nv, nullptr); break;
-      case KALL:
-        hipLaunchKernelGGL((k_backward<DT, M, false, false, KALL>), gr, b, 0, s, q, P, table, g, gt, gq, nk, nv,
-                           nullptr);
-        break;
-      default: hipLaunchKernelGGL((k_backward<DT, M, false, false, NB>), gr, b, 0, s, q, P, table, g, gt, gq, nk, nv, nullptr); break;
-    }
-    return launched();
-  }
-};
-
 int forward_impl(const float* in, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype, int64_t N,
                  int32_t m, void* out, bool th, hipStream_t stream) {
   int64_t L;
@@ -354,9 +352,10 @@ int forward_impl(const float* in, int64_t B, int64_t H, const int32_t K[8], cons
 
 int resolve_mode(int64_t B, int64_t H, int mode, int* resolved);
 
+// width: list width (NB for lram_backward and the activation layer).
 int backward_impl(const float* in, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
                   int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_in, int mode,
-                  void* workspace, size_t ws_bytes, bool th, hipStream_t stream) {
+                  void* workspace, size_t ws_bytes, int width, bool th, hipStream_t stream) {
   int64_t L;
   Params P;
   int rc = check_common(in, B, H, K, &L, &P);
@@ -364,21 +363,22 @@ int backward_impl(const float* in, int64_t B, int64_t H, const int32_t K[8], con
   rc = check_table(table, dtype, N, m, P, L);
   if (rc) return rc;
   if ((rc = resolve_mode(B, H, mode, &mode))) return rc;
+  if (mode == LRAM_SCATTER_SORTED && width != NB) return LRAM_EMODE;  // the sorted scatter takes k = 32
   if (L == 0) return LRAM_OK;
   if (!grad_out || misaligned16(grad_out)) return LRAM_EINVAL;
   if (!grad_table && !grad_in) return LRAM_EINVAL;
   if (grad_table && misaligned16(grad_table)) return LRAM_EINVAL;
   if (grad_in && misaligned16(grad_in)) return LRAM_EINVAL;
   if (mode == LRAM_SCATTER_ATOMIC)
-    return dispatch<BwdAtomicLaunch>(dtype, m, in, P, table, grad_out, grad_table, grad_in, th, stream);
-  if (L > INT64_MAX / NB || L * NB >= (int64_t(1) << 32)) return LRAM_EINVAL;  // positions are 32-bit
+    return dispatch<BwdAtomicLaunch>(dtype, m, in, P, table, grad_out, grad_table, grad_in, th, width, stream);
   if (mode == LRAM_SCATTER_MERGED) {
     const size_t need = merge_ws_layout(L, nullptr, nullptr);
     if (!workspace || ws_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LRAM_EWORKSPACE;
     MergeWs ws;
     merge_ws_layout(L, &ws, reinterpret_cast<char*>(workspace));
-    return dispatch<BwdMergedLaunch>(dtype, m, in, P, table, grad_out, grad_table, grad_in, ws, th, stream);
+    return dispatch<BwdMergedLaunch>(dtype, m, in, P, table, grad_out, grad_table, grad_in, ws, th, width, stream);
   }
+  if (L * NB >= (int64_t(1) << 32)) return LRAM_EINVAL;  // the sorted scatter's pair positions are 32-bit
   const size_t need = sort_ws_layout(L, nullptr, nullptr);
   if (!workspace || ws_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LRAM_EWORKSPACE;
   SortWs ws;
@@ -473,14 +473,14 @@ int lram_backward(const float* q, int64_t B, int64_t H, const int32_t K[8], cons
                   int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_q, int mode,
                   void* workspace, size_t ws_bytes, void* stream) {
   return backward_impl(q, B, H, K, table, dtype, N, m, grad_out, grad_table, grad_q, mode, workspace, ws_bytes,
-                       false, (hipStream_t)stream);
+                       NB, false, (hipStream_t)stream);
 }
 
 int lram_theta_backward(const float* z, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
                         int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_z, int mode,
                         void* workspace, size_t ws_bytes, void* stream) {
   return backward_impl(z, B, H, K, table, dtype, N, m, grad_out, grad_table, grad_z, mode, workspace, ws_bytes,
-                       true, (hipStream_t)stream);
+                       NB, true, (hipStream_t)stream);
 }
 
 int lram_access_histogram(const float* q, int64_t B, int64_t H, const int32_t K[8], float* hist, void* stream) {
@@ -574,21 +574,11 @@ int lram_forward_k(const float* q, int64_t B, int64_t H, const int32_t K[8], con
 
 int lram_backward_k(const float* q, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
                     int64_t N, int32_t m, int32_t k, const float* grad_out, float* grad_table, float* grad_q,
-                    void* stream) {
+                    int mode, void* workspace, size_t ws_bytes, void* stream) {
   const int width = list_width(k);
   if (!width) return LRAM_EINVAL;
-  int64_t L;
-  Params P;
-  int rc = check_common(q, B, H, K, &L, &P);
-  if (rc) return rc;
-  rc = check_table(table, dtype, N, m, P, L);
-  if (rc) return rc;
-  if (L == 0) return LRAM_OK;
-  if (!grad_out || misaligned16(grad_out)) return LRAM_EINVAL;
-  if (!grad_table && !grad_q) return LRAM_EINVAL;
-  if (grad_table && misaligned16(grad_table)) return LRAM_EINVAL;
-  if (grad_q && misaligned16(grad_q)) return LRAM_EINVAL;
-  return dispatch<BwdKLaunch>(dtype, m, q, P, table, grad_out, grad_table, grad_q, width, (hipStream_t)stream);
+  return backward_impl(q, B, H, K, table, dtype, N, m, grad_out, grad_table, grad_q, mode, workspace, ws_bytes,
+                       width, false, (hipStream_t)stream);
 }
 
 }  // extern "C"

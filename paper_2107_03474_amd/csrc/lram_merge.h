@@ -9,10 +9,11 @@ namespace {
 
 // ---------------------------------------------------------------------------
 // Batch-merged scatter.  Lookups whose queries share the closest lattice point
-// share most of their 32 neighbours; the lookups are ordered by that point's
+// share most of their neighbours; the lookups are ordered by that point's
 // location (radix sort above), the backward emits (location, w) pairs in that
-// order, and each batch of MERGE_T consecutive lookups is reduced in LDS to one
-// fp32 atomic row per distinct location of the batch.
+// order, and each batch of consecutive lookups (64; fewer for lists longer
+// than 32, see merge_t) is reduced in LDS to one fp32 atomic row per distinct
+// location of the batch.
 
 // key[l] = location of the closest point of Lambda to q_l (N for a non-finite
 // query), val[l] = (l, 0).
@@ -71,27 +72,34 @@ __global__ void __launch_bounds__(THREADS) k_count_shared(const uint32_t* __rest
 }
 
 constexpr int64_t AUTO_MERGE_MIN = 131072;      // LRAM_SCATTER_AUTO merges from this many lookups on
-constexpr int MERGE_T = 64;                     // lookups per batch (one workgroup)
-constexpr int MERGE_LPW = MERGE_T / WAVES;      // lookups per wave
-constexpr int MERGE_P = MERGE_T * NB;           // pairs per batch
+constexpr int MERGE_P = 64 * NB;                // pair slots per batch
 constexpr int MERGE_H = 2 * MERGE_P;            // hash entries (load factor <= 1/2)
 constexpr int MERGE_HBITS = 12;
 static_assert((1 << MERGE_HBITS) == MERGE_H, "hash size");
-constexpr int MERGE_PPT = MERGE_P / THREADS;    // pairs per thread
+constexpr int MERGE_PPT = MERGE_P / THREADS;    // pair slots per thread
 constexpr int MERGE_HPT = MERGE_H / THREADS;    // hash entries per thread (consecutive)
 constexpr int32_t MERGE_EMPTY = -1;
-static_assert(MERGE_T <= 256 && MERGE_P < 65536, "batch-local indices are 8 and 16 bits wide");
 
-template <int M>
+// Lookups per batch (one workgroup) for lists of KS neighbours: 64, fewer for
+// longer lists so that a batch never holds more than MERGE_P pairs.
+template <int KS>
+constexpr int merge_t() { return KS <= NB ? 64 : MERGE_P / KS; }
+template <int KS>
+constexpr int merge_lpw() { return merge_t<KS>() / WAVES; }
+static_assert(merge_t<16>() * 16 <= MERGE_P && merge_t<KALL>() * KALL <= MERGE_P && merge_lpw<KALL>() >= 1,
+              "batch sizes");
+static_assert(MERGE_P < 65536, "batch-local positions are 16 bits wide");
+
+template <int M, int T>
 struct alignas(16) MergeWork {
   int32_t tag[MERGE_H];         // location of each hash entry; later pair weights and lookups in group order
   uint32_t cnt[MERGE_H / 2];    // 16-bit pair count of each entry, then its first position in group order
-  float g[MERGE_T][M];          // upstream gradient rows of the batch
+  float g[T][M];                // upstream gradient rows of the batch
   uint32_t wsum[WAVES][2];
   uint32_t ngroups;
 };
 
-template <int M>
+template <int M, int KS>
 struct alignas(16) FusedLds {
   union {
     struct {
@@ -104,21 +112,22 @@ struct alignas(16) FusedLds {
     } grp;
   } a;
   union {
-    SearchLds<MERGE_LPW> search;
-    MergeWork<M> merge;
+    SearchLds<merge_lpw<KS>(), KS> search;
+    MergeWork<M, merge_t<KS>()> merge;
   } b;
 };
 
-// One workgroup = one batch of MERGE_T consecutive positions of the order
-// perm: each wave searches MERGE_LPW lookups (with dq as in k_backward) and
-// leaves their (location, w) pairs in LDS; then the workgroup hashes the
-// pairs by location, lays them out grouped by location, and M lanes per
-// distinct location sum w * G over its pairs and add the row with fp32 atomics.
+// One workgroup = one batch of merge_t<KS>() consecutive positions of the
+// order perm: each wave searches merge_lpw<KS>() lookups (with dq as in
+// k_backward) and leaves their (location, w) pairs -- KS per lookup, padding
+// included -- in LDS; then the workgroup hashes the pairs by location, lays
+// them out grouped by location, and M lanes per distinct location sum w * G
+// over its pairs and add the row with fp32 atomics.
 // Several workgroups per CU overlap one's search with another's atomics.
 // A batch in which fewer than a tenth of the lookups share their closest
 // point with a neighbour in the order (queries spread thinly over the torus)
 // has little to merge: it scatters with per-lookup atomics instead.
-template <int DT, int M, bool TH>
+template <int DT, int M, bool TH, int KS = NB>
 __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __restrict__ q, Params P,
                                                              const void* __restrict__ table,
                                                              const float* __restrict__ gout,
@@ -126,7 +135,7 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
                                                              const uint32_t* __restrict__ skey,
                                                              const uint2* __restrict__ perm,
                                                              const uint32_t* __restrict__ gate) {
-  __shared__ FusedLds<M> S;
+  __shared__ FusedLds<M, KS> S;
   if (!merge_chosen(*gate, P.L)) return;  // the batch is scattered by k_backward instead
   const int t = threadIdx.x, wave = t / WAVE, lane = t % WAVE;
   const int64_t bbase = xcd_block() * (WAVES * P.lpw);  // consecutive batches share an L2
@@ -141,8 +150,8 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
     const int64_t base = bbase + (int64_t)wave * P.lpw;
     const int nl = (int)max<int64_t>(0, min<int64_t>(P.lpw, P.L - base));
     if (nl > 0) {
-      Search<NB> srch(P, S.b.search.tab, S.b.search.wave[wave], wave, lane);
-      WaveLds<NB>& W = S.b.search.wave[wave];
+      Search<KS> srch(P, S.b.search.tab, S.b.search.wave[wave], wave, lane);
+      WaveLds<KS>& W = S.b.search.wave[wave];
       Frame* FR = S.b.search.frames[wave];
       const uint32_t my_l = phase_a_perm<TH>(q, perm, base, nl, P, FR, lane);
       const char* tb = reinterpret_cast<const char*>(table);
@@ -151,12 +160,15 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
         const Sel sel = read_sel(F);
         const int count = srch.run(F, sel, 0);
         const int64_t l = (int64_t)__builtin_amdgcn_readlane(my_l, i);
-        if (!merge && count > 0) scatter_atomic<M, NB>(W, count, gout, l, gtab, lane);
-        if (gq) grad_query<DT, M, TH, NB>(F, W, S.b.search.tab, count, tb, gout, l, lane, gq, q, P);
-        if (merge && lane < NB) {
-          const int pidx = (wave * P.lpw + i) * NB + lane;
-          S.a.pairs.loc[pidx] = W.nbr[0][lane].slot;
-          S.a.pairs.w[pidx] = W.wgt[0][lane];
+        if (!merge && count > 0) scatter_atomic<M, KS>(W, count, gout, l, gtab, lane);
+        if (gq) grad_query<DT, M, TH, KS>(F, W, S.b.search.tab, count, tb, gout, l, lane, gq, q, P);
+        if (merge) {
+#pragma unroll
+          for (int j = lane; j < KS; j += WAVE) {
+            const int pidx = (wave * P.lpw + i) * KS + j;
+            S.a.pairs.loc[pidx] = W.nbr[0][j].slot;
+            S.a.pairs.w[pidx] = W.wgt[0][j];
+          }
         }
         wave_lds_sync();
       }
@@ -164,7 +176,7 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
   }
   if (!merge) return;  // uniform across the workgroup
   __syncthreads();
-  MergeWork<M>& MW = S.b.merge;
+  MergeWork<M, merge_t<KS>()>& MW = S.b.merge;
 #pragma unroll
   for (int k = 0; k < MERGE_HPT; ++k) MW.tag[k * THREADS + t] = MERGE_EMPTY;
 #pragma unroll
@@ -183,7 +195,7 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
     const int pidx = k * THREADS + t;
     ent[k] = 0xFFFFFFFFu;
     wv[k] = 0.0f;
-    if (pidx < nt * NB) {
+    if (pidx < nt * KS) {
       const int32_t loc = S.a.pairs.loc[pidx];
       wv[k] = S.a.pairs.w[pidx];
       if (loc >= 0) {
@@ -261,7 +273,7 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
       const uint32_t h = ent[k] & 0xFFFFu;
       const uint32_t pos = ((MW.cnt[h >> 1] >> (16u * (h & 1u))) & 0xFFFFu) + (ent[k] >> 16);
       pw[pos] = wv[k];
-      pt[pos] = (uint8_t)((k * THREADS + t) / NB);
+      pt[pos] = (uint8_t)((k * THREADS + t) / KS);
     }
   }
   __syncthreads();

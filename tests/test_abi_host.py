@@ -126,8 +126,17 @@ def test_variable_k_validation(lib):
     assert lib.lram_forward_k(FAKE, 4, 1, K4, FAKE, 0, 4 ** 8, 32, -1, FAKE, None) == 1
     assert lib.lram_neighbors_k(FAKE, 4, 1, K4, 128, FAKE, FAKE, None, None) == 1
     assert lib.lram_neighbors_k(FAKE, 4, 1, (ctypes.c_int32 * 8)(*([5] * 8)), 0, FAKE, FAKE, None, None) == 2
-    assert lib.lram_backward_k(FAKE, 4, 1, K4, FAKE, 0, 4 ** 8, 32, 16, None, FAKE, FAKE, None) == 1
-    assert lib.lram_backward_k(FAKE, 4, 1, K4, FAKE, 0, 4 ** 8, 40, 16, FAKE, FAKE, FAKE, None) == 3
+    def bwd_k(k=16, m=32, grad_out=FAKE, mode=0, ws=None, wsb=0):
+        return lib.lram_backward_k(FAKE, 4, 1, K4, FAKE, 0, 4 ** 8, m, k, grad_out, FAKE, FAKE, mode, ws, wsb, None)
+
+    assert bwd_k(grad_out=None) == 1
+    assert bwd_k(m=40) == 3
+    assert bwd_k(k=48) == 1
+    assert bwd_k(mode=1) == 5                      # the sorted scatter takes k = 32 only
+    assert bwd_k(k=0, mode=1) == 5
+    assert bwd_k(mode=2) == 4                      # merged without a workspace
+    assert bwd_k(k=64, mode=2, ws=FAKE_MIS, wsb=1 << 20) == 4
+    assert bwd_k(mode=7) == 5
     assert lib.lram_forward_k(None, 0, 1, K4, None, 0, 4 ** 8, 32, 0, None, None) == 0
 
 

@@ -35,10 +35,17 @@ def _rel_rows(a, b):
     return np.where(den > 0, num / np.where(den > 0, den, 1), num)
 
 
-def _queries(K, L, seed):
+def _queries(K, L, seed, clustered=False):
+    """Uniform queries (or, clustered, around 16 centres so that lookups share
+    their closest lattice point and the merged scatter merges), plus special
+    ones: next to lattice points, rounding-admitted shells, a lattice point, a
+    deep hole and a NaN (row 242)."""
     rng = np.random.default_rng(seed)
     Kf = np.asarray(K, np.float64)
     q = rng.random((L, 8)) * Kf
+    if clustered:
+        centres = rng.random((16, 8)) * Kf
+        q = np.mod(centres[rng.integers(0, 16, L)] + 0.3 * rng.standard_normal((L, 8)), Kf)
     q[:200] = np.mod(rng.integers(0, 4, (200, 8)) * 0.5 + rng.standard_normal((200, 8)) * 1e-3, Kf)  # near points
     t = np.float32(3.801106e-08) * np.arange(1, 41, dtype=np.float32)   # rounding admits shell points
     q[200:240] = np.repeat(t[:, None], 8, axis=1)
@@ -63,13 +70,16 @@ def test_neighbors_k(K, k):
         assert nb["count"].max() > 121  # the rounding-admitted shell is exercised
 
 
+@pytest.mark.parametrize("mode,clustered", [("atomic", False), ("merged", False), ("merged", True)])
 @pytest.mark.parametrize("k", KS)
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("m", [32, 64])
 @pytest.mark.parametrize("K", [(4,) * 8, (2, 4, 6, 8, 2, 4, 6, 8)])
-def test_forward_backward_k(K, m, dtype, k):
-    _say("fwd/bwd k=%d K=%s m=%d %s" % (k, K, m, dtype))
-    q_np = _queries(K, 2500, 32)
+def test_forward_backward_k(K, m, dtype, k, mode, clustered):
+    """mode merged with uniform queries: the device gate falls back to the
+    atomic kernel; with clustered queries the batches are merged."""
+    _say("fwd/bwd k=%d K=%s m=%d %s %s%s" % (k, K, m, dtype, mode, " clustered" if clustered else ""))
+    q_np = _queries(K, 2500, 32, clustered)
     q = torch.from_numpy(q_np).to(DEV)
     N = int(np.prod(K))
     gen = torch.Generator(device=DEV)
@@ -77,7 +87,7 @@ def test_forward_backward_k(K, m, dtype, k):
     table = (torch.randn((N, m), device=DEV, generator=gen) * 0.02).to(dtype)
     G = torch.randn((q_np.shape[0], m), device=DEV, generator=gen)
     out = lram.forward(q, table, K, k=k)
-    gt, gq = lram.backward(q, table, K, G, k=k)
+    gt, gq = lram.backward(q, table, K, G, k=k, mode=mode)
     torch.cuda.synchronize()
     nb = oracle.neighbors(q_np, K, k=k)
     rows = oracle.gather_rows(table.float().cpu().numpy(), nb["slot"])
