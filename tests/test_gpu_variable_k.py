@@ -134,3 +134,39 @@ def test_coverage_grows_with_k():
     _say("coverage", cov)
     assert cov[16] < cov[32] < cov[64] <= 1.0
     assert abs(cov[32] - 0.995) < 0.002
+
+
+@pytest.mark.parametrize("k", KS)
+def test_merged_at_scale(k):
+    """Clustered batches large enough that the merged kernel runs at its
+    per-wave caps (16, 8 and 2 lookups per wave for k = 16, 64 and the whole
+    support; the plain kernels take L / 4096 per wave): every touched gradient
+    row against the oracle's fp64 sums, dq on a sample, untouched rows exactly 0."""
+    K = (8,) * 8
+    N = 8 ** 8
+    L = {16: 65536 + 77, 64: 32768 + 77, 0: 16384 + 77}[k]   # ragged: the last batch is partial
+    _say("merged at scale k=%d" % k)
+    rng = np.random.default_rng(40 + k)
+    centres = rng.random((512, 8)) * 8
+    rank = rng.zipf(1.1, L) % 512
+    q_np = np.mod(centres[rank] + 0.3 * rng.standard_normal((L, 8)), 8.0).astype(np.float32)
+    q = torch.from_numpy(q_np).to(DEV)
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(9)
+    table = torch.randn((N, 32), device=DEV, generator=gen) * 0.02
+    G = torch.randn((L, 32), device=DEV, generator=gen)
+    gt, gq = lram.backward(q, table, K, G, k=k, mode="merged")
+    torch.cuda.synchronize()
+    nb = oracle.neighbors(q_np, K, k=k)
+    Gn = G.cpu().numpy()
+    uniq, acc = oracle.grad_table_rows(nb, Gn, weights="w32")
+    dV = gt.cpu().numpy()
+    assert _rel_rows(dV[uniq], acc).max() <= 1e-5
+    mask = np.ones(N, bool)
+    mask[uniq] = False
+    assert np.all(dV[mask] == 0)
+    sample = rng.choice(L, 4096, replace=False)
+    nbs = {key: v[sample] for key, v in nb.items()}
+    rows = oracle.gather_rows(table.cpu().numpy(), nbs["slot"])
+    err = _rel_rows(gq.cpu().numpy()[sample], oracle.grad_query(nbs, rows, Gn[sample]))
+    assert err.max() <= 1e-5, err.max()
