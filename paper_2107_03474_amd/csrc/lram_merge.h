@@ -80,14 +80,23 @@ constexpr int MERGE_PPT = MERGE_P / THREADS;    // pair slots per thread
 constexpr int MERGE_HPT = MERGE_H / THREADS;    // hash entries per thread (consecutive)
 constexpr int32_t MERGE_EMPTY = -1;
 
-// Lookups per batch (one workgroup) for lists of KS neighbours: 64, fewer for
-// longer lists so that a batch never holds more than MERGE_P pairs.
+// Pair layout of a batch.  Fixed: lookup b's list of KS entries (padding
+// included) fills slots [b KS, (b+1) KS).  Compact (the untruncated lookup,
+// whose lists are up to 241 long but 65 on average): each wave owns MERGE_SEG
+// slots and appends its lookups' real pairs there; a lookup that no longer
+// fits scatters with per-lookup atomics instead.
 template <int KS>
-constexpr int merge_t() { return KS <= NB ? 64 : MERGE_P / KS; }
+constexpr bool merge_compact() { return KS == KALL; }
+constexpr int MERGE_SEG = MERGE_P / WAVES;
+
+// Lookups per batch (one workgroup) for lists of KS neighbours: 64, fewer for
+// longer fixed lists so that a batch never holds more than MERGE_P pairs, 32
+// for the compact layout.
+template <int KS>
+constexpr int merge_t() { return merge_compact<KS>() ? 32 : (KS <= NB ? 64 : MERGE_P / KS); }
 template <int KS>
 constexpr int merge_lpw() { return merge_t<KS>() / WAVES; }
-static_assert(merge_t<16>() * 16 <= MERGE_P && merge_t<KALL>() * KALL <= MERGE_P && merge_lpw<KALL>() >= 1,
-              "batch sizes");
+static_assert(merge_t<16>() * 16 <= MERGE_P && merge_t<64>() * 64 <= MERGE_P && KALL <= MERGE_SEG, "batch sizes");
 static_assert(MERGE_P < 65536, "batch-local positions are 16 bits wide");
 
 template <int M, int T>
@@ -103,8 +112,9 @@ template <int M, int KS>
 struct alignas(16) FusedLds {
   union {
     struct {
-      int32_t loc[MERGE_P];     // (location, w) of every pair, [lookup in batch][j]
+      int32_t loc[MERGE_P];     // (location, w) of every pair (-1: empty slot)
       float w[MERGE_P];
+      uint8_t lk[merge_compact<KS>() ? MERGE_P : 1];  // compact layout: the pair's lookup in the batch
     } pairs;
     struct {
       int32_t loc[MERGE_P];     // distinct locations of the batch
@@ -146,6 +156,8 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
     shared = (t > 0 && skey[bbase + t - 1] == k) || (t + 1 < nt && skey[bbase + t + 1] == k);
   }
   const bool merge = 10 * __syncthreads_count(shared) >= nt;
+  constexpr bool COMPACT = merge_compact<KS>();
+  int used = 0;  // compact layout: slots of this wave's segment taken (wave-uniform)
   {
     const int64_t base = bbase + (int64_t)wave * P.lpw;
     const int nl = (int)max<int64_t>(0, min<int64_t>(P.lpw, P.L - base));
@@ -162,7 +174,7 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
         const int64_t l = (int64_t)__builtin_amdgcn_readlane(my_l, i);
         if (!merge && count > 0) scatter_atomic<M, KS>(W, count, gout, l, gtab, lane);
         if (gq) grad_query<DT, M, TH, KS>(F, W, S.b.search.tab, count, tb, gout, l, lane, gq, q, P);
-        if (merge) {
+        if (merge && !COMPACT) {
 #pragma unroll
           for (int j = lane; j < KS; j += WAVE) {
             const int pidx = (wave * P.lpw + i) * KS + j;
@@ -170,11 +182,27 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
             S.a.pairs.w[pidx] = W.wgt[0][j];
           }
         }
+        if constexpr (COMPACT) {
+          if (merge && used + count <= MERGE_SEG) {
+            for (int j = lane; j < count; j += WAVE) {
+              const int pidx = wave * MERGE_SEG + used + j;
+              S.a.pairs.loc[pidx] = W.nbr[0][j].slot;
+              S.a.pairs.w[pidx] = W.wgt[0][j];
+              S.a.pairs.lk[pidx] = (uint8_t)(wave * P.lpw + i);
+            }
+            used += count;
+          } else if (merge && count > 0) {
+            scatter_atomic<M, KS>(W, count, gout, l, gtab, lane);  // the segment is full
+          }
+        }
         wave_lds_sync();
       }
     }
   }
   if (!merge) return;  // uniform across the workgroup
+  if constexpr (COMPACT) {
+    for (int j = used + lane; j < MERGE_SEG; j += WAVE) S.a.pairs.loc[wave * MERGE_SEG + j] = -1;
+  }
   __syncthreads();
   MergeWork<M, merge_t<KS>()>& MW = S.b.merge;
 #pragma unroll
@@ -190,14 +218,17 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
   // insert every pair's location; keep (entry, rank among the entry's pairs)
   uint32_t ent[MERGE_PPT];
   float wv[MERGE_PPT];
+  uint8_t lkv[MERGE_PPT];
 #pragma unroll
   for (int k = 0; k < MERGE_PPT; ++k) {
     const int pidx = k * THREADS + t;
     ent[k] = 0xFFFFFFFFu;
     wv[k] = 0.0f;
-    if (pidx < nt * KS) {
+    lkv[k] = (uint8_t)(pidx / KS);
+    if (pidx < (COMPACT ? MERGE_P : nt * KS)) {
       const int32_t loc = S.a.pairs.loc[pidx];
       wv[k] = S.a.pairs.w[pidx];
+      if constexpr (COMPACT) lkv[k] = S.a.pairs.lk[pidx];
       if (loc >= 0) {
         uint32_t h = ((uint32_t)loc * 0x9E3779B1u) >> (32 - MERGE_HBITS);
         while (true) {
@@ -273,7 +304,7 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
       const uint32_t h = ent[k] & 0xFFFFu;
       const uint32_t pos = ((MW.cnt[h >> 1] >> (16u * (h & 1u))) & 0xFFFFu) + (ent[k] >> 16);
       pw[pos] = wv[k];
-      pt[pos] = (uint8_t)((k * THREADS + t) / KS);
+      pt[pos] = lkv[k];
     }
   }
   __syncthreads();
