@@ -244,7 +244,7 @@ int merged_pass(const float* q, const Params& P, const void* table, const float*
   if (int rc = radix_sort(ws.sort, P.N, s, &keys, &perm)) return rc;
   hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(WAVE), 0, s, ws.shared, 0u);
   const int64_t cb = (P.L + THREADS - 1) / THREADS;
-  hipLaunchKernelGGL(k_count_shared, dim3((unsigned)(cb < 2048 ? cb : 2048)), dim3(THREADS), 0, s,
+  hipLaunchKernelGGL(k_count_shared, dim3((unsigned)(cb < 512 ? cb : 512)), dim3(THREADS), 0, s,
                      (const uint32_t*)keys, P.L, ws.shared);
   launch_atomic<DT, M, TH, KS>(q, P, table, g, gt, gq, ws.shared, s);
   if (int rc = launched()) return rc;

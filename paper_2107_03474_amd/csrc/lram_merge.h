@@ -58,9 +58,11 @@ __global__ void k_fill_u32(uint32_t* __restrict__ p, uint32_t v) {
   if (threadIdx.x == 0) *p = v;
 }
 
-// *count += number of positions whose sorted key equals a neighbour's.
+// *count += number of positions whose sorted key equals a neighbour's (one
+// atomic per workgroup: same-address atomics serialise in memory).
 __global__ void __launch_bounds__(THREADS) k_count_shared(const uint32_t* __restrict__ keys, int64_t L,
                                                           uint32_t* __restrict__ count) {
+  __shared__ uint32_t part[WAVES];
   uint32_t c = 0;
   for (int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x; i < L; i += (int64_t)gridDim.x * THREADS) {
     const uint32_t k = keys[i];
@@ -68,7 +70,14 @@ __global__ void __launch_bounds__(THREADS) k_count_shared(const uint32_t* __rest
   }
 #pragma unroll
   for (int mask = 1; mask < WAVE; mask <<= 1) c += __shfl_xor(c, mask);
-  if (threadIdx.x % WAVE == 0 && c) atomicAdd(count, c);
+  if (threadIdx.x % WAVE == 0) part[threadIdx.x / WAVE] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t t = 0;
+#pragma unroll
+    for (int w = 0; w < WAVES; ++w) t += part[w];
+    if (t) atomicAdd(count, t);
+  }
 }
 
 constexpr int64_t AUTO_MERGE_MIN = 131072;      // LRAM_SCATTER_AUTO merges from this many lookups on
@@ -308,15 +317,37 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
     }
   }
   __syncthreads();
-  // one row per distinct location: M lanes (lane = column) sum w * G over its pairs
+  // one row per distinct location: M lanes (lane = column) sum w * G over its
+  // pairs.  A lane takes U locations at a time and reads their first pairs
+  // together (most locations have one or two pairs), so those LDS reads
+  // overlap; further pairs follow location by location.
   constexpr int GROUPS = THREADS / M;
+  constexpr int U = 4;
   const int col = t % M;
   const uint32_t ngroups = MW.ngroups;
-  for (uint32_t gi = t / M; gi < ngroups; gi += GROUPS) {
-    const uint32_t p0 = S.a.grp.start[gi], p1 = S.a.grp.start[gi + 1];
-    float acc = 0.0f;
-    for (uint32_t p = p0; p < p1; ++p) acc = fmaf(pw[p], MW.g[pt[p]][col], acc);
-    unsafeAtomicAdd(gtab + (size_t)S.a.grp.loc[gi] * M + col, acc);
+  for (uint32_t g0 = t / M; g0 < ngroups; g0 += U * GROUPS) {
+    uint32_t p0[U], p1[U];
+    int32_t loc[U];
+    float acc[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t gi = g0 + u * GROUPS;
+      const bool ok = gi < ngroups;
+      p0[u] = ok ? S.a.grp.start[gi] : 0u;
+      p1[u] = ok ? S.a.grp.start[gi + 1] : 0u;
+      loc[u] = ok ? S.a.grp.loc[gi] : -1;
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t p = p0[u] < p1[u] ? p0[u] : 0u;
+      acc[u] = fmaf(pw[p], MW.g[pt[p]][col], 0.0f);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      for (uint32_t p = p0[u] + 1; p < p1[u]; ++p) acc[u] = fmaf(pw[p], MW.g[pt[p]][col], acc[u]);
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (loc[u] >= 0) unsafeAtomicAdd(gtab + (size_t)loc[u] * M + col, acc[u]);
   }
 }
 
