@@ -108,11 +108,19 @@ constexpr int merge_lpw() { return merge_t<KS>() / WAVES; }
 static_assert(merge_t<16>() * 16 <= MERGE_P && merge_t<64>() * 64 <= MERGE_P && KALL <= MERGE_SEG, "batch sizes");
 static_assert(MERGE_P < 65536, "batch-local positions are 16 bits wide");
 
+// LDS of the fused kernel, two regions whose contents change from phase to phase.
+// Region a: the batch's (location, w) pairs while the search runs; then the
+// hash table's location tags; then, compacted to its front, the distinct
+// locations in group order, with the pair weights in group order in its upper
+// half.  Region b: the search; then the hash entries' pair counts (later their
+// first positions in group order), the upstream gradient rows of the batch,
+// the groups' first positions and the pairs' lookups in group order.
 template <int M, int T>
 struct alignas(16) MergeWork {
-  int32_t tag[MERGE_H];         // location of each hash entry; later pair weights and lookups in group order
   uint32_t cnt[MERGE_H / 2];    // 16-bit pair count of each entry, then its first position in group order
   float g[T][M];                // upstream gradient rows of the batch
+  uint16_t start[MERGE_P + 2];  // first position of each group (location) in group order
+  uint8_t pt[MERGE_P];          // lookup (in the batch) of each pair, in group order
   uint32_t wsum[WAVES][2];
   uint32_t ngroups;
 };
@@ -125,16 +133,14 @@ struct alignas(16) FusedLds {
       float w[MERGE_P];
       uint8_t lk[merge_compact<KS>() ? MERGE_P : 1];  // compact layout: the pair's lookup in the batch
     } pairs;
-    struct {
-      int32_t loc[MERGE_P];     // distinct locations of the batch
-      uint16_t start[MERGE_P + 2];  // first position of each location's pairs in group order
-    } grp;
+    int32_t tag[MERGE_H];       // hash tags; then group locations [0, ngroups) and pair weights [MERGE_P, 2 MERGE_P)
   } a;
   union {
     SearchLds<merge_lpw<KS>(), KS> search;
     MergeWork<M, merge_t<KS>()> merge;
   } b;
 };
+static_assert(MERGE_H == 2 * MERGE_P, "group locations and pair weights share the tag array");
 
 // One workgroup = one batch of merge_t<KS>() consecutive positions of the
 // order perm: each wave searches merge_lpw<KS>() lookups (with dq as in
@@ -213,9 +219,27 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
     for (int j = used + lane; j < MERGE_SEG; j += WAVE) S.a.pairs.loc[wave * MERGE_SEG + j] = -1;
   }
   __syncthreads();
-  MergeWork<M, merge_t<KS>()>& MW = S.b.merge;
+  // this thread's pairs into registers: region a then takes the hash tags
+  int32_t locv[MERGE_PPT];
+  float wv[MERGE_PPT];
+  uint8_t lkv[MERGE_PPT];
 #pragma unroll
-  for (int k = 0; k < MERGE_HPT; ++k) MW.tag[k * THREADS + t] = MERGE_EMPTY;
+  for (int k = 0; k < MERGE_PPT; ++k) {
+    const int pidx = k * THREADS + t;
+    locv[k] = -1;
+    wv[k] = 0.0f;
+    lkv[k] = (uint8_t)(pidx / KS);
+    if (pidx < (COMPACT ? MERGE_P : nt * KS)) {
+      locv[k] = S.a.pairs.loc[pidx];
+      wv[k] = S.a.pairs.w[pidx];
+      if constexpr (COMPACT) lkv[k] = S.a.pairs.lk[pidx];
+    }
+  }
+  __syncthreads();
+  MergeWork<M, merge_t<KS>()>& MW = S.b.merge;
+  int32_t* tag = S.a.tag;
+#pragma unroll
+  for (int k = 0; k < MERGE_HPT; ++k) tag[k * THREADS + t] = MERGE_EMPTY;
 #pragma unroll
   for (int k = 0; k < MERGE_HPT / 2; ++k) MW.cnt[k * THREADS + t] = 0u;
   for (int i = t; i < nt * (M / 4); i += THREADS) {
@@ -226,35 +250,29 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
   __syncthreads();
   // insert every pair's location; keep (entry, rank among the entry's pairs)
   uint32_t ent[MERGE_PPT];
-  float wv[MERGE_PPT];
-  uint8_t lkv[MERGE_PPT];
 #pragma unroll
   for (int k = 0; k < MERGE_PPT; ++k) {
-    const int pidx = k * THREADS + t;
     ent[k] = 0xFFFFFFFFu;
-    wv[k] = 0.0f;
-    lkv[k] = (uint8_t)(pidx / KS);
-    if (pidx < (COMPACT ? MERGE_P : nt * KS)) {
-      const int32_t loc = S.a.pairs.loc[pidx];
-      wv[k] = S.a.pairs.w[pidx];
-      if constexpr (COMPACT) lkv[k] = S.a.pairs.lk[pidx];
-      if (loc >= 0) {
-        uint32_t h = ((uint32_t)loc * 0x9E3779B1u) >> (32 - MERGE_HBITS);
-        while (true) {
-          const int32_t old = atomicCAS(&MW.tag[h], MERGE_EMPTY, loc);
-          if (old == MERGE_EMPTY || old == loc) break;
-          h = (h + 1) & (MERGE_H - 1);
-        }
-        const uint32_t sh = 16u * (h & 1u);
-        const uint32_t rank = (atomicAdd(&MW.cnt[h >> 1], 1u << sh) >> sh) & 0xFFFFu;
-        ent[k] = h | (rank << 16);
+    const int32_t loc = locv[k];
+    if (loc >= 0) {
+      uint32_t h = ((uint32_t)loc * 0x9E3779B1u) >> (32 - MERGE_HBITS);
+      while (true) {
+        const int32_t old = atomicCAS(&tag[h], MERGE_EMPTY, loc);
+        if (old == MERGE_EMPTY || old == loc) break;
+        h = (h + 1) & (MERGE_H - 1);
       }
+      const uint32_t sh = 16u * (h & 1u);
+      const uint32_t rank = (atomicAdd(&MW.cnt[h >> 1], 1u << sh) >> sh) & 0xFFFFu;
+      ent[k] = h | (rank << 16);
     }
   }
   __syncthreads();
   // exclusive scan over the entries: group index and first position of each
-  // occupied entry (this thread owns entries [t*HPT, (t+1)*HPT))
+  // occupied entry (this thread owns entries [t*HPT, (t+1)*HPT)); the owned
+  // tags are read now, before the group locations overwrite the front of the
+  // tag array
   uint32_t c[MERGE_HPT];
+  int32_t tg[MERGE_HPT];
   uint32_t ng = 0, np = 0;
 #pragma unroll
   for (int k = 0; k < MERGE_HPT / 2; ++k) {
@@ -264,6 +282,7 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
   }
 #pragma unroll
   for (int k = 0; k < MERGE_HPT; ++k) {
+    tg[k] = tag[t * MERGE_HPT + k];
     ng += c[k] ? 1u : 0u;
     np += c[k];
   }
@@ -288,15 +307,15 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
   }
   if (t == THREADS - 1) {
     MW.ngroups = gb + ng;
-    S.a.grp.start[gb + ng] = (uint16_t)(pb + np);
+    MW.start[gb + ng] = (uint16_t)(pb + np);
   }
   uint32_t first[MERGE_HPT];
 #pragma unroll
   for (int k = 0; k < MERGE_HPT; ++k) {
     first[k] = pb;
     if (c[k]) {
-      S.a.grp.loc[gb] = MW.tag[t * MERGE_HPT + k];
-      S.a.grp.start[gb] = (uint16_t)pb;
+      tag[gb] = tg[k];  // group gb's location; gb <= entry index, every tag already read
+      MW.start[gb] = (uint16_t)pb;
       ++gb;
       pb += c[k];
     }
@@ -304,9 +323,9 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
 #pragma unroll
   for (int k = 0; k < MERGE_HPT / 2; ++k) MW.cnt[t * (MERGE_HPT / 2) + k] = first[2 * k] | (first[2 * k + 1] << 16);
   __syncthreads();
-  // pairs into group order (over the dead hash tags)
-  float* pw = reinterpret_cast<float*>(MW.tag);
-  uint8_t* pt = reinterpret_cast<uint8_t*>(MW.tag + MERGE_P);
+  // pairs into group order: weights in the upper half of the tag array
+  float* pw = reinterpret_cast<float*>(tag + MERGE_P);
+  uint8_t* pt = MW.pt;
 #pragma unroll
   for (int k = 0; k < MERGE_PPT; ++k) {
     if (ent[k] != 0xFFFFFFFFu) {
@@ -333,9 +352,9 @@ __global__ void __launch_bounds__(THREADS) k_backward_merged(const float* __rest
     for (int u = 0; u < U; ++u) {
       const uint32_t gi = g0 + u * GROUPS;
       const bool ok = gi < ngroups;
-      p0[u] = ok ? S.a.grp.start[gi] : 0u;
-      p1[u] = ok ? S.a.grp.start[gi + 1] : 0u;
-      loc[u] = ok ? S.a.grp.loc[gi] : -1;
+      p0[u] = ok ? MW.start[gi] : 0u;
+      p1[u] = ok ? MW.start[gi + 1] : 0u;
+      loc[u] = ok ? tag[gi] : -1;
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
