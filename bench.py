@@ -93,10 +93,13 @@ def cpu_baseline(oracle, W, w, q_np, table, G, target_s, torch):
             break
         n = int(min(qf.shape[0], max(2 * n, n * target_s / max(t, 1e-3))))
     cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    # the enumeration runs on `cores` OpenMP threads; numpy's einsum, unique and
+    # add.at run on one thread
     return {"value": n / t, "unit": "lookups/s (fwd+bwd)", "cores": cores, "kind": "oracle", "cpu": cpu_model(),
-            "sample": "%d random lookups of the %s batch (%.1f s: neighbour enumeration %.1f s in C/OpenMP, "
-                      "fp64 gather/grad algebra %.1f s in numpy; rows copied from the GPU table untimed)"
-                      % (n, w.name, t, t_nb, t_alg)}
+            "threads": {"neighbour_enumeration": cores, "fp64_algebra": 1},
+            "sample": "%d random lookups of the %s batch (%.1f s: neighbour enumeration %.1f s in C on %d OpenMP "
+                      "threads, fp64 gather/grad algebra %.1f s in single-threaded numpy; rows copied from the GPU "
+                      "table untimed)" % (n, w.name, t, t_nb, cores, t_alg)}
 
 
 def measured_traffic(workload: str, kernel: str):

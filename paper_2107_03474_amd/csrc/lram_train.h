@@ -85,7 +85,9 @@ __global__ void __launch_bounds__(THREADS) k_sparse_adam(void* __restrict__ tabl
   constexpr int RW = WAVE / M;  // rows per wave
   const int lane = threadIdx.x % WAVE;
   const int col = lane % M, sub = lane / M;
-  const uint64_t seg = (M == WAVE) ? ~0ull : (((1ull << M) - 1ull) << (M * sub));
+  // lanes of this lane's row in a wave-wide ballot
+  constexpr uint64_t row_mask = M == WAVE ? ~0ull : (1ull << (M % WAVE)) - 1ull;
+  const uint64_t seg = row_mask << (M * sub);
   const int64_t waves = (int64_t)gridDim.x * WAVES;
   for (int64_t rb = ((int64_t)blockIdx.x * WAVES + threadIdx.x / WAVE) * RW; rb < N; rb += waves * RW) {
     const int64_t r = rb + sub;
