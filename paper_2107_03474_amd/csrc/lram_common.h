@@ -71,11 +71,12 @@ struct alignas(16) Nbr {
   int32_t slot;       // location, -1 for padding
 };
 
-// Per-wave search state for lists of KS neighbours.
-template <int KS>
+// Per-wave search state for lists of KS neighbours, NBUF lists deep (the k =
+// 32 forward double-buffers them: lookup t+1 is searched while t is consumed).
+template <int KS, int NBUF = 1>
 struct alignas(16) WaveLds {
-  Nbr nbr[2][KS];     // double-buffered: lookup t+1 is searched while t is consumed
-  float wgt[2][KS];
+  Nbr nbr[NBUF][KS];
+  float wgt[NBUF][KS];
   uint32_t tie[tie_max<KS>()][2];
   uint32_t hist[64];  // distance histogram of the selection, 64 buckets on [4, 8)
 };
@@ -88,10 +89,10 @@ struct alignas(16) Tables {
 };
 
 // LDS of the search for FR lookups per wave and lists of KS neighbours.
-template <int FR, int KS = NB>
+template <int FR, int KS = NB, int NBUF = 1>
 struct alignas(16) SearchLds {
   Tables tab;
-  WaveLds<KS> wave[WAVES];
+  WaveLds<KS, NBUF> wave[WAVES];
   Frame frames[WAVES][FR];
 };
 

@@ -113,8 +113,8 @@ struct FwdGeom {
 };
 
 // Loads the rows r0 .. r0 + R of list `buf` (R = the geometry's chunk).
-template <int DT, int M, int KS, int R = NB>
-__device__ __forceinline__ void fwd_issue(const char* __restrict__ tb, const WaveLds<KS>& W, int buf, int lane,
+template <int DT, int M, int KS, int R = NB, int NBUF = 1>
+__device__ __forceinline__ void fwd_issue(const char* __restrict__ tb, const WaveLds<KS, NBUF>& W, int buf, int lane,
                                           uint32_t (&v)[FwdGeom<DT, M, R>::NI][FwdGeom<DT, M, R>::DW], int r0 = 0) {
   using G = FwdGeom<DT, M, R>;
   const int rsub = lane / G::LPR, col = lane % G::LPR;
@@ -133,8 +133,8 @@ __device__ __forceinline__ void fwd_issue(const char* __restrict__ tb, const Wav
 }
 
 // acc += sum over the rows r0 .. r0 + R of w_j * v_j (this lane's columns).
-template <int DT, int M, int KS, int R = NB>
-__device__ __forceinline__ void fwd_accumulate(const WaveLds<KS>& W, int buf, int lane,
+template <int DT, int M, int KS, int R = NB, int NBUF = 1>
+__device__ __forceinline__ void fwd_accumulate(const WaveLds<KS, NBUF>& W, int buf, int lane,
                                                const uint32_t (&v)[FwdGeom<DT, M, R>::NI][FwdGeom<DT, M, R>::DW],
                                                float (&acc)[FwdGeom<DT, M, R>::EPL], int r0 = 0) {
   using G = FwdGeom<DT, M, R>;
@@ -179,7 +179,7 @@ __device__ __forceinline__ void fwd_store(int lane, int64_t l, float (&acc)[FwdG
 }
 
 template <int DT, int M>
-__device__ __forceinline__ void fwd_consume(const WaveLds<NB>& W, int buf, int lane, int64_t l,
+__device__ __forceinline__ void fwd_consume(const WaveLds<NB, 2>& W, int buf, int lane, int64_t l,
                                             const uint32_t (&v)[FwdGeom<DT, M>::NI][FwdGeom<DT, M>::DW],
                                             void* __restrict__ out) {
   float acc[FwdGeom<DT, M>::EPL];
@@ -195,11 +195,11 @@ template <int DT, int M, bool TH>
 __global__ void __launch_bounds__(THREADS) k_forward(const float* __restrict__ q, Params P,
                                                      const void* __restrict__ table, void* __restrict__ out) {
   using G = FwdGeom<DT, M>;
-  __shared__ SearchLds<WAVE> S;
+  __shared__ SearchLds<WAVE, NB, 2> S;
   WaveCtx c;
   if (!wave_ctx(P, c)) return;
-  Search<NB> srch(P, S.tab, S.wave[c.wave], c.wave, c.lane);
-  WaveLds<NB>& W = S.wave[c.wave];
+  Search<NB, 2> srch(P, S.tab, S.wave[c.wave], c.wave, c.lane);
+  WaveLds<NB, 2>& W = S.wave[c.wave];
   Frame* FR = S.frames[c.wave];
   phase_a<TH>(q, c.base, c.nl, P, FR, c.lane);
   const char* tb = reinterpret_cast<const char*>(table);

@@ -143,11 +143,13 @@ struct alignas(16) FusedLds {
 static_assert(MERGE_H == 2 * MERGE_P, "group locations and pair weights share the tag array");
 
 // Waves per SIMD that the LDS of one batch allows (160 KB per CU, 4 SIMDs):
-// the register budget is held to it, so registers never lower the occupancy
-// below what the LDS permits.
-template <int M, int KS>
+// the register budget is held to it, so registers do not lower the occupancy
+// below what the LDS permits -- except for fp32 tables with m = 64, whose
+// 256-byte rows need more registers than four waves per SIMD leave.
+template <int DT, int M, int KS>
 constexpr int merge_waves_per_simd() {
-  return (int)((160 * 1024) / sizeof(FusedLds<M, KS>)) * WAVES / 4;
+  const int w = (int)((160 * 1024) / sizeof(FusedLds<M, KS>)) * WAVES / 4;
+  return (DT == LRAM_F32 && M == 64 && w > 3) ? 3 : w;
 }
 
 // One workgroup = one batch of merge_t<KS>() consecutive positions of the
@@ -161,7 +163,7 @@ constexpr int merge_waves_per_simd() {
 // point with a neighbour in the order (queries spread thinly over the torus)
 // has little to merge: it scatters with per-lookup atomics instead.
 template <int DT, int M, bool TH, int KS = NB>
-__global__ void __launch_bounds__(THREADS, (merge_waves_per_simd<M, KS>())) k_backward_merged(const float* __restrict__ q, Params P,
+__global__ void __launch_bounds__(THREADS, (merge_waves_per_simd<DT, M, KS>())) k_backward_merged(const float* __restrict__ q, Params P,
                                                              const void* __restrict__ table,
                                                              const float* __restrict__ gout,
                                                              float* __restrict__ gtab, float* __restrict__ gq,

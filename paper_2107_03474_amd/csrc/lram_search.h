@@ -355,10 +355,10 @@ __device__ __forceinline__ int threshold_k_hist(const uint32_t (&key)[NS], uint3
   return ks;
 }
 
-template <int KS>
+template <int KS, int NBUF = 1>
 struct Search {
   Tables& S;
-  WaveLds<KS>& W;
+  WaveLds<KS, NBUF>& W;
   int lane;
   uint32_t wbyte;
   uint32_t lo[NS_STRICT], hi[NS_STRICT];
@@ -369,7 +369,7 @@ struct Search {
 
   // (the kernel argument is read field by field: holding a reference to it
   // would force the argument block into private memory)
-  __device__ Search(const Params P, Tables& s, WaveLds<KS>& wv, int w, int l)
+  __device__ Search(const Params P, Tables& s, WaveLds<KS, NBUF>& wv, int w, int l)
       : S(s), W(wv), lane(l), wbyte(64u * (uint32_t)w) {
 #pragma unroll
     for (int k = 0; k < NS_STRICT; ++k) load_candidate<0>(lane + WAVE * k, wbyte, lo[k], hi[k]);
