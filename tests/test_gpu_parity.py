@@ -296,6 +296,42 @@ def test_mixed_batches_merged():
     assert np.all(dV[mask] == 0)
 
 
+def test_merged_batches_near_capacity():
+    """Merged scatter on batches whose lookups are mostly spread thinly but
+    share their closest lattice point often enough (two in five) for the merge
+    to run: about 1,600 distinct locations among a batch's 2,048 pairs, so the
+    group locations compacted over the hash tags and the pair weights in the
+    tags' upper half nearly fill their halves; three full batches and a ragged one."""
+    _say("merged batches near capacity")
+    K = (8,) * 8
+    rng = np.random.default_rng(21)
+    npair, nsingle = 42, 127
+    base = rng.random((npair, 8)) * 8
+    twins = np.mod(base + 1e-3 * rng.standard_normal((npair, 8)), 8)
+    q_np = np.concatenate([base, twins, rng.random((nsingle, 8)) * 8]).astype(np.float32)
+    q_np = q_np[rng.permutation(q_np.shape[0])]
+    L = q_np.shape[0]
+    assert L == 3 * 64 + 19
+    q = torch.from_numpy(q_np).to(DEV)
+    table = _small_table(K, 32, torch.float32)
+    G = torch.randn((L, 32), device=DEV)
+    gt, gq = lram.backward(q, table, K, G, mode="merged")
+    gta, gqa = lram.backward(q, table, K, G, mode="atomic")
+    torch.cuda.synchronize()
+    assert torch.equal(gq, gqa)
+    nb = oracle.neighbors(q_np, K)
+    cells = nb["slot"][:, 0]
+    assert np.unique(cells).size <= L - npair + 2  # the twins share their cell
+    uniq, acc = oracle.grad_table_rows(nb, G.cpu().numpy())
+    assert uniq.size > 0.75 * 32 * L
+    dV = gt.cpu().numpy()
+    assert _rel_rows(dV[uniq], acc).max() <= 1e-5
+    mask = np.ones(dV.shape[0], bool)
+    mask[uniq] = False
+    assert np.all(dV[mask] == 0)
+    assert _rel_rows(dV[uniq], gta.cpu().numpy()[uniq]).max() <= 1e-5
+
+
 @pytest.mark.parametrize("mode", ["sorted", "merged"])
 def test_workspace_errors(mode):
     K = (4,) * 8
