@@ -75,7 +75,8 @@ typedef enum {
   LRAM_SCATTER_ATOMIC = 0, /* fp32 atomic adds straight into grad_table */
   LRAM_SCATTER_SORTED = 1, /* sort (slot, lookup) pairs, one read-modify-write per touched row */
   LRAM_SCATTER_MERGED = 2, /* order lookups by their closest lattice point, merge equal slots within
-                              each batch of 64 consecutive lookups, one atomic row per distinct slot;
+                              each batch of consecutive lookups (64 for lists of up to 32, 32 for
+                              longer ones), one atomic row per distinct slot;
                               when fewer than a tenth of the lookups share their closest point with
                               another (nothing to merge) the device falls back to the atomic scatter */
   LRAM_SCATTER_AUTO = 3    /* MERGED for L >= 131072 lookups, ATOMIC below (the sort does not pay off) */
