@@ -150,6 +150,8 @@ def main():
     ap.add_argument("--no-subnetwork", action="store_true", help="skip timing the memory subnetwork slice")
     ap.add_argument("--no-training", action="store_true", help="skip the access statistics and the Adam step")
     ap.add_argument("--no-graph", action="store_true", help="skip the small-batch eager vs graph-replay timing")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip timing the other full-size workloads (K = 8 fp32 m = 64, K = 12 bf16 m = 64)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy 5 times (HBM counter calibration)")
     args = ap.parse_args()
@@ -378,15 +380,84 @@ def main():
         log("cpu baseline (oracle) ...")
         res["cpu_baseline"] = cpu_baseline(oracle, W, w, q_np, table, G, args.cpu_seconds, torch)
         log("cpu baseline done")
+    del table, gtab, G, out, gq, q
+    torch.cuda.empty_cache()
+    if not args.no_workloads:
+        res["workloads"] = time_workloads(torch, lram, W, log)
     if not args.no_subnetwork:
-        del table, gtab, G, out, gq, q
-        torch.cuda.empty_cache()
         res["memory_subnetwork"] = time_subnetwork(torch, lram, log)
     if not args.no_training:
         res["training"] = time_training(torch, lram, W, log)
     if not args.no_graph:
         res["small_batch_graph"] = time_small_graph(torch, lram, W, log)
     print(json.dumps(res), flush=True)
+
+
+def time_workloads(torch, lram, W, log, reps=10):
+    """The other full-size workloads, timed like the headline one (not part of
+    `value`): k8-m64-f32-uniform (forward only: 256-byte fp32 rows, whole
+    lines) and k12-m64-bf16-proj (forward + backward, 128-byte rows, queries
+    from a dense projection), each with its requested bytes (every lookup
+    reads its 32 rows) and compulsory bytes (each distinct row once) per
+    second, and the requested rate as a fraction of the 8 TB/s peak."""
+    dev = torch.device("cuda")
+    stream = torch.cuda.current_stream()
+    out = {}
+
+    def timed(f):
+        f()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            f()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    for name in ("k8-m64-f32-uniform", "k12-m64-bf16-proj"):
+        w, fits = pick_workload(W, name, torch)
+        if not fits:
+            out[name] = None
+            continue
+        q = torch.from_numpy(W.queries(w)).to(dev)
+        table = W.make_table(w, dev)
+        o = torch.empty((w.B, w.H, w.m), dtype=table.dtype, device=dev)
+        U = unique_rows(lram, q, w.K, torch)
+        st = 4 if w.dtype == "f32" else 2
+        L = w.L
+        fwd_ms = timed(lambda: lram.forward(q, table, w.K, out=o))
+        fwd_req = L * (32 + 32 * w.m * st + w.m * st)
+        fwd_comp = L * (32 + w.m * st) + U * w.m * st
+        rec = {"lookups": L, "locations": w.N, "m": w.m, "table_dtype": w.dtype, "distinct_rows": U,
+               "fwd_ms": fwd_ms, "fwd_lookups_per_s": L / (fwd_ms * 1e-3),
+               "fwd_requested_GBps": fwd_req / (fwd_ms * 1e-3) / 1e9,
+               "fwd_requested_frac": fwd_req / (fwd_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+               "fwd_hbm_GBps": fwd_comp / (fwd_ms * 1e-3) / 1e9}
+        if w.backward:
+            G = W.grad_out(w, dev)
+            gtab = torch.zeros((w.N, w.m), dtype=torch.float32, device=dev)
+            gq = torch.empty((w.B, w.H, 8), dtype=torch.float32, device=dev)
+            mode = lram.resolved_mode(w.B, w.H, "auto")
+            nws = lram.backward_workspace_bytes(w.B, w.H, w.m, mode)
+            ws = torch.empty(nws, dtype=torch.uint8, device=dev) if nws else None
+            bwd_ms = timed(lambda: lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, mode=mode,
+                                                 workspace=ws))
+            bwd_req = L * (32 + w.m * 4 + 32 + 32 * (w.m * st + 2 * w.m * 4))
+            bwd_comp = L * (32 + w.m * 4 + 32) + U * (w.m * st + 2 * w.m * 4)
+            rec.update({"scatter": mode, "bwd_ms": bwd_ms, "lookups_per_s": L / ((fwd_ms + bwd_ms) * 1e-3),
+                        "bwd_requested_GBps": bwd_req / (bwd_ms * 1e-3) / 1e9,
+                        "bwd_requested_frac": bwd_req / (bwd_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                        "bwd_hbm_GBps": bwd_comp / (bwd_ms * 1e-3) / 1e9})
+            del G, gtab, gq, ws
+        out[name] = rec
+        log("%s: forward %.3f ms (%.0f GB/s requested)%s" % (
+            name, fwd_ms, rec["fwd_requested_GBps"],
+            ", backward %.3f ms (%.0f GB/s requested)" % (rec["bwd_ms"], rec["bwd_requested_GBps"])
+            if w.backward else ""))
+        del q, table, o
+        torch.cuda.empty_cache()
+    return out
 
 
 def time_small_graph(torch, lram, W, log, reps=200):
