@@ -362,6 +362,11 @@ struct Search {
   int lane;
   uint32_t wbyte;
   uint32_t lo[NS_STRICT], hi[NS_STRICT];
+  // the untruncated lookup scans the boundary candidates every time: they stay
+  // in registers too (the truncated ones read them from constant memory on
+  // the rare path that needs them)
+  static constexpr int NB_REG = KS == KALL ? NS_BOUND : 1;
+  uint32_t blo[NB_REG], bhi[NB_REG];
   // lane constants of the table build: coordinate i = lane/8, value v = lane%8
   int ti, tp, tK;
   uint32_t tS, tN0;
@@ -373,6 +378,10 @@ struct Search {
       : S(s), W(wv), lane(l), wbyte(64u * (uint32_t)w) {
 #pragma unroll
     for (int k = 0; k < NS_STRICT; ++k) load_candidate<0>(lane + WAVE * k, wbyte, lo[k], hi[k]);
+    if constexpr (KS == KALL) {
+#pragma unroll
+      for (int k = 0; k < NS_BOUND; ++k) load_candidate<1>(lane + WAVE * k, wbyte, blo[k], bhi[k]);
+    }
     ti = lane >> 3;
     tp = (lane & 7) + CMIN;
     tK = P.K[0];
@@ -392,6 +401,9 @@ struct Search {
     if (s < NS_STRICT) {
       l = lo[s];
       h = hi[s];
+    } else if constexpr (KS == KALL) {
+      l = blo[s - NS_STRICT];
+      h = bhi[s - NS_STRICT];
     } else {
       load_candidate<1>(lane + WAVE * (s - NS_STRICT), wbyte, l, h);
     }
@@ -501,11 +513,18 @@ struct Search {
         uint32_t key7[NS_ALL];
 #pragma unroll
         for (int k = 0; k < NS_STRICT; ++k) key7[k] = key[k];
+        if constexpr (KS == KALL) {
+#pragma unroll
+          for (int k = 0; k < NS_BOUND; ++k)
+            key7[NS_STRICT + k] = (lane + WAVE * k < E8_NBOUNDARY) ? __float_as_uint(cand_d2(S.qt, blo[k], bhi[k], sel))
+                                                                   : KEY_INF;
+        } else {
 #pragma unroll 1
-        for (int k = 0; k < NS_BOUND; ++k) {
-          uint32_t l, h;
-          const bool okb = load_candidate<1>(lane + WAVE * k, wbyte, l, h);
-          key7[NS_STRICT + k] = okb ? __float_as_uint(cand_d2(S.qt, l, h, sel)) : KEY_INF;
+          for (int k = 0; k < NS_BOUND; ++k) {
+            uint32_t l, h;
+            const bool okb = load_candidate<1>(lane + WAVE * k, wbyte, l, h);
+            key7[NS_STRICT + k] = okb ? __float_as_uint(cand_d2(S.qt, l, h, sel)) : KEY_INF;
+          }
         }
         if constexpr (KS == KALL) {
           // untruncated: every candidate whose recipe distance is below 8
