@@ -362,10 +362,11 @@ struct Search {
   int lane;
   uint32_t wbyte;
   uint32_t lo[NS_STRICT], hi[NS_STRICT];
-  // the untruncated lookup scans the boundary candidates every time: they stay
-  // in registers too (the truncated ones read them from constant memory on
-  // the rare path that needs them)
-  static constexpr int NB_REG = KS == KALL ? NS_BOUND : 1;
+  // lists of 64 and the untruncated lookup scan the boundary candidates often
+  // (whenever the support holds fewer than 64 points) or always: they stay in
+  // registers too (shorter lists read them from constant memory on the rare
+  // path that needs them)
+  static constexpr int NB_REG = KS >= 64 ? NS_BOUND : 1;
   uint32_t blo[NB_REG], bhi[NB_REG];
   // lane constants of the table build: coordinate i = lane/8, value v = lane%8
   int ti, tp, tK;
@@ -378,7 +379,7 @@ struct Search {
       : S(s), W(wv), lane(l), wbyte(64u * (uint32_t)w) {
 #pragma unroll
     for (int k = 0; k < NS_STRICT; ++k) load_candidate<0>(lane + WAVE * k, wbyte, lo[k], hi[k]);
-    if constexpr (KS == KALL) {
+    if constexpr (NB_REG == NS_BOUND) {
 #pragma unroll
       for (int k = 0; k < NS_BOUND; ++k) load_candidate<1>(lane + WAVE * k, wbyte, blo[k], bhi[k]);
     }
@@ -401,7 +402,7 @@ struct Search {
     if (s < NS_STRICT) {
       l = lo[s];
       h = hi[s];
-    } else if constexpr (KS == KALL) {
+    } else if constexpr (NB_REG == NS_BOUND) {
       l = blo[s - NS_STRICT];
       h = bhi[s - NS_STRICT];
     } else {
@@ -513,7 +514,7 @@ struct Search {
         uint32_t key7[NS_ALL];
 #pragma unroll
         for (int k = 0; k < NS_STRICT; ++k) key7[k] = key[k];
-        if constexpr (KS == KALL) {
+        if constexpr (NB_REG == NS_BOUND) {
 #pragma unroll
           for (int k = 0; k < NS_BOUND; ++k)
             key7[NS_STRICT + k] = (lane + WAVE * k < E8_NBOUNDARY) ? __float_as_uint(cand_d2(S.qt, blo[k], bhi[k], sel))
