@@ -130,3 +130,79 @@ def test_full_size(name):
     del table, gtab, G, out, slot, wgt, d2, all_touched
     gc.collect()
     torch.cuda.empty_cache()
+
+
+def test_full_size_theta():
+    """The activation layer in front of the billion-location lookup, as the
+    benchmark's `theta` leg runs it (merged scatter): torus coordinates of
+    sampled lookups bit-exact, their outputs (bf16 table: 2e-2) and grad_z
+    (1e-5), sampled gradient rows against the oracle's fp64 sums over the
+    whole batch (1e-4), untouched rows exactly 0."""
+    name = "k14-m32-bf16-zipf"
+    w = W.WORKLOADS[name]
+    gc.collect()
+    torch.cuda.empty_cache()
+    ok, need, free = _fits(w)
+    if not ok:
+        pytest.skip("needs %.1f GB of device memory, %.1f GB free" % (need / 1e9, free / 1e9))
+    _say("full size theta", name, "- building inputs")
+    z_np = W.theta_inputs(w)
+    z = torch.from_numpy(z_np).to(DEV)
+    table = W.make_table(w, DEV)
+    G = W.grad_out(w, DEV)
+    gtab = torch.zeros((w.N, w.m), dtype=torch.float32, device=DEV)
+    out = lram.theta_forward(z, table, w.K)
+    _, gz = lram.theta_backward(z, table, w.K, G, grad_table=gtab)
+    torch.cuda.synchronize()
+    _say("kernels done")
+
+    rng = np.random.default_rng(2025)
+    zf = z_np.reshape(-1, 16)
+    idx = np.sort(rng.choice(w.L, 4096, replace=False))
+    ti = torch.from_numpy(idx).to(DEV)
+    q, s = oracle.theta_coords(zf[idx], w.K)
+    qg, sg = lram.theta_coords(z.reshape(-1, 16)[ti].contiguous(), w.K)
+    np.testing.assert_array_equal(qg.cpu().numpy().view(np.uint32), q.view(np.uint32))
+    nb = oracle.neighbors(q, w.K)
+    rows = _rows(table, nb["slot"])
+    err = _rel_rows(out.reshape(-1, w.m)[ti].float().cpu().numpy(), oracle.theta_forward(nb, rows, s))
+    _say("theta out: max rel err %.2e" % err.max())
+    assert err.max() <= 2e-2
+    Gf = G.reshape(-1, w.m)
+    gz_ref = oracle.theta_grad_z(zf[idx], w.K, nb, rows, s, Gf[ti].cpu().numpy())
+    err = _rel_rows(gz.reshape(-1, 16)[ti].cpu().numpy(), gz_ref)
+    _say("grad_z: max rel err %.2e" % err.max())
+    assert err.max() <= 1e-5
+
+    touched = np.unique(nb["slot"][nb["slot"] >= 0])
+    pick = np.sort(rng.choice(touched, min(1024, touched.size), replace=False))
+    acc = np.zeros((pick.size, w.m), np.float64)
+    G_host = Gf.cpu().numpy()
+    chunk = 1 << 18
+    for s0 in range(0, w.L, chunk):
+        s1 = min(w.L, s0 + chunk)
+        qc, sc = oracle.theta_coords(zf[s0:s1], w.K)
+        nbc = oracle.neighbors(qc, w.K)
+        sl = nbc["slot"]
+        hit = np.isin(sl, pick)
+        if hit.any():
+            li, ji = np.nonzero(hit)
+            pos = np.searchsorted(pick, sl[li, ji])
+            np.add.at(acc, pos, (nbc["w64"][li, ji] * sc[li])[:, None] * G_host[s0 + li].astype(np.float64))
+        del nbc
+        gc.collect()
+        _say("oracle gradient rows: %d / %d lookups" % (s1, w.L))
+    err = _rel_rows(gtab[torch.from_numpy(pick).to(DEV)].cpu().numpy(), acc)
+    _say("dV: max rel err %.2e over %d sampled rows" % (err.max(), pick.size))
+    assert err.max() <= 1e-4
+    cand = torch.from_numpy(rng.choice(w.N, 4096, replace=False)).to(DEV)
+    slot, _, _ = lram.neighbors(lram.theta_coords(z, w.K)[0], w.K, want_d2=False)
+    all_touched = torch.zeros(w.N, dtype=torch.bool, device=DEV)
+    sv = slot.reshape(-1)
+    all_touched[sv[sv >= 0].long()] = True
+    cold = cand[~all_touched[cand]]
+    assert cold.numel() > 100
+    assert torch.count_nonzero(gtab[cold]).item() == 0
+    del table, gtab, G, out, gz, z, slot, all_touched
+    gc.collect()
+    torch.cuda.empty_cache()
