@@ -118,13 +118,17 @@ __device__ __forceinline__ void grad_query(const Frame& F, const WaveLds<KS>& W,
     for (int k = 0; k < ICOORD; ++k) dq[k] += __shfl_xor(dq[k], mask);
     if constexpr (TH) dls += __shfl_xor(dls, mask);
   }
-  if (rsub == 0) {
+  // every lane of column ch now holds the sums; lane (rsub, ch) with rsub <
+  // ICOORD writes coordinate ch + rsub*LPR, so the coordinates' epilogues run
+  // side by side rather than one after another
+  if (rsub < ICOORD) {
+    double dqk = dq[0];
 #pragma unroll
-    for (int k = 0; k < ICOORD; ++k) {
-      const int i = ch + k * G::LPR;
-      if (i >= 8) continue;
+    for (int k = 1; k < ICOORD; ++k) dqk = rsub == k ? dq[k] : dqk;
+    const int i = ch + rsub * G::LPR;
+    if (i < 8) {
       if constexpr (!TH) {
-        gq[l * 8 + i] = (float)dq[k];
+        gq[l * 8 + i] = (float)dqk;
       } else {
         double ci = P.cK[0];
 #pragma unroll
@@ -135,10 +139,10 @@ __device__ __forceinline__ void grad_query(const Frame& F, const WaveLds<KS>& W,
           const float2 ab = *reinterpret_cast<const float2*>(zin + l * 16 + 2 * i);
           const double a = ab.x, b = ab.y;
           const double r2 = a * a + b * b;
-          const double r3 = r2 * sqrt(r2);
-          const double ds = dls * sc * sc, dqs = dq[k] * sc * ci;
-          ga = ds * a / r3 - dqs * b / r2;
-          gb = ds * b / r3 + dqs * a / r2;
+          const double ir2 = 1.0 / r2, ir3 = ir2 / sqrt(r2);  // 1/r^2, 1/r^3
+          const double ds = dls * sc * sc, dqs = dqk * sc * ci;
+          ga = ds * a * ir3 - dqs * b * ir2;
+          gb = ds * b * ir3 + dqs * a * ir2;
         }
         *reinterpret_cast<float2*>(gq + l * 16 + 2 * i) = make_float2((float)ga, (float)gb);
       }
