@@ -24,7 +24,10 @@ import test_oracle_invariance as inv
 import test_oracle_locations as locs
 import test_oracle_pins as pins
 import test_oracle_theta as th
+import test_oracle_subnetwork as subt
 import test_oracle_training as tr
+import test_oracle_variable_k as vk
+from oracle import subnetwork
 
 _SRC = os.path.join(os.path.dirname(oracle.__file__), "lram_oracle.c")
 _counter = itertools.count()
@@ -53,13 +56,13 @@ def _plant_c(monkeypatch, tmp_path, old, new):
     monkeypatch.setattr(oracle, "_lib", None)
 
 
-def _plant_py(monkeypatch, name, old, new):
-    """Replaces oracle.<name> by its own source with one edit."""
-    src = inspect.getsource(getattr(oracle, name))
+def _plant_py(monkeypatch, name, old, new, module=oracle):
+    """Replaces module.<name> by its own source with one edit."""
+    src = inspect.getsource(getattr(module, name))
     assert src.count(old) == 1, (name, old)
-    ns = dict(vars(oracle))
-    exec(compile(src.replace(old, new), "<mutant of oracle.%s>" % name, "exec"), ns)
-    monkeypatch.setattr(oracle, name, ns[name])
+    ns = dict(vars(module))
+    exec(compile(src.replace(old, new), "<mutant of %s.%s>" % (module.__name__, name), "exec"), ns)
+    monkeypatch.setattr(module, name, ns[name])
 
 
 def _first_failure(battery):
@@ -119,6 +122,22 @@ def _theta_battery():
     ]
 
 
+def _variable_k_battery():
+    return [
+        ("closest k are prefixes", vk.test_closest_k_are_prefixes),
+        ("untruncated total weight", vk.test_untruncated_total_weight),
+        ("rounding-admitted shell", vk.test_rounding_can_admit_the_shell_but_never_beyond_it),
+        ("whole support against the brute force at K = 4", lambda: vk.test_whole_support_matches_bruteforce((4,) * 8)),
+    ]
+
+
+def _subnetwork_battery():
+    return [
+        ("identity dense parts reduce to theta", subt.test_identity_dense_parts_reduce_to_theta),
+        ("gradients against finite differences", subt.test_gradients_match_directional_finite_differences),
+    ]
+
+
 def _training_battery():
     return [
         ("Adam = torch.optim.Adam", tr.test_adam_matches_torch_when_every_row_is_touched),
@@ -172,6 +191,22 @@ PY_CORE_MUTANTS = {
     "table gradient overwrites": ("grad_table_rows", "np.add.at(acc, inv, contrib)", "acc[inv] = contrib"),
     "table gradient without weights": ("grad_table_rows", "contrib = (w[:, :, None] * Gf[:, None, :])[valid]",
                                        "contrib = (np.ones_like(w)[:, :, None] * Gf[:, None, :])[valid]"),
+}
+
+C_VARIABLE_K_MUTANTS = {
+    # Sec. 2.2 / 2.5: the untruncated sum runs over the whole support
+    "whole support cut at 121 points": ("      if (j < c.n) {", "      if (j < c.n && j < 121) {"),
+}
+
+PY_SUBNETWORK_MUTANTS = {
+    # Sec. 3.1: y = W2 theta(BN(W1 x + b1)) + b2
+    "first dense layer transposed": ("forward", 'pre = x @ p["W1"].T + p["b1"]', 'pre = x @ p["W1"] + p["b1"]'),
+    "batch norm without the square root": ("forward", 'inv = 1.0 / np.sqrt(p["var"] + p["eps"])',
+                                           'inv = 1.0 / (p["var"] + p["eps"])'),
+    "gamma gradient from the unnormalised features": ("backward", 'norm = (st["pre"] - p["mu"]) * st["inv"]',
+                                                      'norm = st["pre"] - p["mu"]'),
+    "pre-activation gradient without the normalisation": ("backward", 'dpre = dz * p["gamma"] * st["inv"]',
+                                                          'dpre = dz * p["gamma"]'),
 }
 
 PY_THETA_MUTANTS = {
@@ -248,6 +283,29 @@ def test_training_mutant_is_caught(name, monkeypatch):
     assert caught is not None, name
 
 
+@pytest.mark.parametrize("name", sorted(C_VARIABLE_K_MUTANTS))
+def test_variable_k_mutant_is_caught(name, monkeypatch, tmp_path):
+    _plant_c(monkeypatch, tmp_path, *C_VARIABLE_K_MUTANTS[name])
+    caught = _first_failure(_variable_k_battery())
+    print("%s: caught by %s" % (name, caught))
+    assert caught is not None, name
+
+
+@pytest.mark.parametrize("name", sorted(PY_SUBNETWORK_MUTANTS))
+def test_subnetwork_mutant_is_caught(name, monkeypatch):
+    _plant_py(monkeypatch, *PY_SUBNETWORK_MUTANTS[name], module=subnetwork)
+    caught = _first_failure(_subnetwork_battery())
+    print("%s: caught by %s" % (name, caught))
+    assert caught is not None, name
+
+
 def test_python_batteries_pass_unmutated():
     assert _first_failure(_theta_battery()) is None
     assert _first_failure(_training_battery()) is None
+    assert _first_failure(_subnetwork_battery()) is None
+
+
+def test_unmutated_c_source_passes_the_variable_k_pins(monkeypatch, tmp_path):
+    monkeypatch.setattr(oracle, "_LIB_PATH", _build_c(tmp_path, open(_SRC).read()))
+    monkeypatch.setattr(oracle, "_lib", None)
+    assert _first_failure(_variable_k_battery()) is None

@@ -78,4 +78,5 @@ def test_rounding_can_admit_the_shell_but_never_beyond_it():
     # the admitted extra points are exactly at distance sqrt 8 in exact arithmetic
     for l in np.nonzero(nb["count"] > 121)[0][:5]:
         n = nb["count"][l]
+        assert np.all(nb["slot"][l, :n] >= 0) and np.all(nb["slot"][l, n:] == -1)  # every point listed
         assert np.all(nb["d64"][l, :n] < 8 + 1e-5)
