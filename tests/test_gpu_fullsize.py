@@ -9,7 +9,9 @@ checks sampled outputs one by one:
   * gradient rows of sampled locations: the oracle accumulates the contribution
     of every lookup of the batch (in chunks) to those rows; per-row relative L2
     <= 1e-4 (fp32 atomics in any order vs fp64, up to ~3e4 terms per hot row);
-  * sampled locations no lookup touches: exactly 0.
+  * sampled locations no lookup touches: exactly 0;
+  * on the billion-location workload the atomic and sorted scatters are run
+    too and checked the same way (dq bit-identical across the three).
 """
 import gc
 
@@ -127,6 +129,20 @@ def test_full_size(name):
     cold = cand[~all_touched[cand]]
     assert cold.numel() > 100
     assert torch.count_nonzero(gtab[cold]).item() == 0
+    if name == "k14-m32-bf16-zipf":
+        # the other two scatters at the same scale, against the same oracle rows
+        pick_t = torch.from_numpy(pick).to(DEV)
+        for mode in ("atomic", "sorted"):
+            gtab.zero_()
+            gq2 = torch.empty_like(gq)
+            lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq2, mode=mode)
+            torch.cuda.synchronize()
+            assert torch.equal(gq2, gq), mode  # dq does not depend on the scatter
+            err = _rel_rows(gtab[pick_t].cpu().numpy(), acc)
+            _say("dV (%s scatter): max rel err %.2e over %d sampled rows" % (mode, err.max(), pick.size))
+            assert err.max() <= 1e-4
+            assert torch.count_nonzero(gtab[cold]).item() == 0
+            del gq2
     del table, gtab, G, out, slot, wgt, d2, all_touched
     gc.collect()
     torch.cuda.empty_cache()
