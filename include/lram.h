@@ -132,12 +132,14 @@ int lram_scatter_mode_resolved(int64_t B, int64_t H, int mode, int* resolved);
  *       (accumulated: the caller zeroes grad_table once; untouched rows are not
  *        written; concurrent calls on other streams that update the same
  *        grad_table race only in rounding order under LRAM_SCATTER_ATOMIC and
- *        must not overlap under LRAM_SCATTER_SORTED)
+ *        LRAM_SCATTER_MERGED, whose row adds are atomic, and must not overlap
+ *        under LRAM_SCATTER_SORTED)
  *   grad_q[l][i] = sum_j -2 u_j^3 (x_i - k_{j,i}) <grad_out[l], table[slot_j]>,
  *       u_j = 1 - s_j/8 (overwritten; nullable to skip it)
  * The neighbour search is recomputed from q.  workspace/ws_bytes: device
  * buffer, 256-byte aligned, of at least lram_backward_workspace_bytes (may be
- * NULL for the atomic mode); its contents on entry do not matter.  The sorted
+ * NULL for the atomic mode); its contents on entry do not matter, and calls
+ * that may overlap need workspaces of their own.  The sorted
  * mode needs 32 L < 2^32.  grad_table may be NULL only if grad_q is not
  * (without grad_table every mode computes grad_q the same way).
  */
