@@ -90,6 +90,7 @@ def _core_battery():
     return [
         ("lattice point returns its value", pins.test_lattice_point_returns_its_value),
         ("deep hole: 16 neighbours of weight 1/16", pins.test_deep_hole_sixteen_sixteenths),
+        ("recipe weight is the kernel", pins.test_recipe_weight_is_the_kernel),
         ("total weight 1 at lattice points and deep holes", pins.test_total_weight_one_at_lattice_points_and_deep_holes),
         ("shell of 240 nearest neighbours", pins.test_nearest_neighbour_shell_is_240),
         ("x is the exact fmod of 2q", bf.test_bruteforce_x_is_exact_fmod),
@@ -160,6 +161,10 @@ C_MUTANTS = {
     # Sec. 2.5: f(r) = (1 - r^2/8)^4
     "kernel cubed": ("  double u2 = u * u;\n  return u2 * u2;", "  double u2 = u * u;\n  return u2 * u;"),
     "kernel radius 2 instead of sqrt 8": ("double u = 1.0 - d2 / 8.0;", "double u = 1.0 - d2 / 4.0;"),
+    # the fp32 recipe weight is the same kernel, u^4
+    "recipe weight cubed": ("w32[o] = u2 * u2;", "w32[o] = u2 * u;"),
+    "recipe weight squared": ("w32[o] = u2 * u2;", "w32[o] = u * u;"),
+    "recipe weight with radius 2": ("float u = 1.0f - r->d * 0.125f;", "float u = 1.0f - r->d * 0.25f;"),
     # Sec. 2.6: the closest 32
     "farthest points first": ("if (bx != by) return bx < by ? -1 : 1;", "if (bx != by) return bx < by ? 1 : -1;"),
     "ties by descending location": ("if (x->slot != y->slot) return x->slot < y->slot ? -1 : 1;",

@@ -153,3 +153,45 @@ def test_nearest_neighbour_shell_is_240():
 
 def test_truncation_never_exceeds_32(mc):
     assert np.all((mc["slot"] >= 0).sum(1) == np.minimum(mc["count"], 32))
+
+
+def test_recipe_weight_is_the_kernel():
+    """Sec. 2.5: the fp32 weight the oracle records beside the fp64 one (the
+    weight the GPU's selection and scatter use) is the kernel
+    f(r) = (1 - r^2/8)^4 of that passage:
+      * exactly 1 at a lattice point, and exactly 1/16 at each of the 16 points
+        around a deep hole (the two special cases Sec. 2.5 names);
+      * on queries of a 2^-3 grid at the doubled scale every squared distance
+        is a multiple of 1/64, so u = 1 - r^2/8 = a/512 and u^2 are exact in
+        fp32 and f(r) = a^4/2^36 is formed by one rounding: the recorded
+        weight equals f(r) computed here from the lattice points in exact
+        integers, rounded once to fp32;
+      * elsewhere it stays within 4e-6 of f(r) taken in fp64 from the query and
+        the listed lattice points (the fp32 differences, squares and sums of
+        r^2 add at most 10 roundings of r^2 <= 8, i.e. 4.8e-6 in r^2, 6e-7 in
+        u, and d(u^4)/du <= 4 over [0, 1], plus two roundings of the powers)."""
+    pts = np.array([[0, 0, 0, 0, 0, 0, 0, 0], [1, 1, 1, 1, 1, 1, 1, 1], [2, 0, 0, 0, 0, 0, 0, 0],
+                    [1, 1, 1, 1, 1, 1, 1, -1]], np.float32) / 2
+    nb = oracle.neighbors(np.mod(pts, 8), K8)
+    assert nb["w32"][0, 0] == 1.0 and nb["w32"][1, 0] == 1.0
+    assert np.all(nb["w32"][:2, 1:] == 0.0)
+    assert np.all(nb["w32"][2:, :16] == np.float32(1.0 / 16)) and np.all(nb["w32"][2:, 16:] == 0.0)
+
+    rng = np.random.default_rng(2107)
+    grid = rng.integers(0, 8 * 16, size=(400, 8))            # x = grid / 8 on [0, 16)
+    nb = oracle.neighbors((grid / 16.0).astype(np.float32), K8)
+    valid = nb["slot"] >= 0
+    e8 = grid[:, None, :] - 8 * nb["lift"].astype(np.int64)   # 8 (x - k), exact integers
+    r2_64 = (e8 * e8).sum(-1)                                  # 64 r^2
+    a = 512 - r2_64                                            # 512 u
+    assert np.all(a[valid] > 0)
+    exact = (a.astype(np.float64) ** 4 / 2.0 ** 36).astype(np.float32)
+    np.testing.assert_array_equal(nb["w32"][valid], exact[valid])
+    assert np.unique(a[valid]).size > 100                      # many distinct weights covered
+
+    q = (rng.random((2000, 8)) * 8).astype(np.float32)
+    nb = oracle.neighbors(q, K8)
+    valid = nb["slot"] >= 0
+    e = nb["x"].astype(np.float64)[:, None, :] - nb["lift"].astype(np.float64)
+    f = (1.0 - (e * e).sum(-1) / 8.0) ** 4
+    assert np.abs(nb["w32"][valid] - f[valid]).max() <= 4e-6
