@@ -16,8 +16,10 @@ average launch time measured with HIP events on its own stream;
 from __future__ import annotations
 
 import argparse
+import ctypes
 import json
 import os
+import subprocess
 import sys
 import time
 
@@ -56,50 +58,110 @@ def unique_rows(lram, q, K, torch):
     return int(seen.numel())
 
 
-def cpu_model() -> str:
+def cpu_info() -> dict:
+    """The host CPU as lscpu reports it (model, sockets, cores, threads)."""
+    info = {}
     try:
-        for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                return line.split(":", 1)[1].strip()
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=30).stdout
+        for line in out.splitlines():
+            k, _, v = line.partition(":")
+            if k.strip() in ("Model name", "Socket(s)", "Core(s) per socket", "Thread(s) per core", "CPU(s)",
+                             "CPU max MHz", "L3"):
+                info[k.strip()] = v.strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    return info
+
+
+def _omp_threads(n):
+    """Thread count of the oracle's OpenMP enumeration for the calling thread."""
+    try:
+        ctypes.CDLL("libgomp.so.1").omp_set_num_threads(int(n))
     except OSError:
         pass
-    return "unknown"
+
+
+def _oracle_pass(oracle, qs, rows, g, K, threads):
+    """The oracle's fwd+bwd on a sample, data-parallel over `threads` threads:
+    the neighbour enumeration (C, OpenMP), then forward, dq and the value
+    gradient of lookup chunks (numpy, which releases the interpreter lock),
+    then the chunks' gradient rows merged per row partition.  Returns seconds."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    n = qs.shape[0]
+    _omp_threads(threads)
+    t0 = time.perf_counter()
+    nb = oracle.neighbors(qs, K)
+    bounds = [(i * n // threads, (i + 1) * n // threads) for i in range(threads)]
+
+    def algebra(b):
+        sl = slice(*b)
+        nbs = {k: v[sl] for k, v in nb.items()}
+        oracle.forward(nbs, rows[sl])
+        oracle.grad_query(nbs, rows[sl], g[sl])
+        return oracle.grad_table_rows(nbs, g[sl])
+
+    def merge(p):
+        us, accs = [], []
+        for u, a in parts:
+            k = (u % threads) == p
+            us.append(u[k])
+            accs.append(a[k])
+        u = np.concatenate(us)
+        uniq, inv = np.unique(u, return_inverse=True)
+        acc = np.zeros((uniq.size, g.shape[1]), np.float64)
+        np.add.at(acc, inv, np.concatenate(accs))
+        return uniq.size
+
+    with ThreadPoolExecutor(threads) as ex:
+        parts = list(ex.map(algebra, bounds))
+        rows_out = sum(ex.map(merge, range(threads)))
+    assert rows_out > 0
+    return time.perf_counter() - t0
 
 
 def cpu_baseline(oracle, W, w, q_np, table, G, target_s, torch):
-    """The oracle on a bounded random sample of the workload's lookups (fwd+bwd)."""
+    """The oracle timed on the host cores: median of 3 passes over a random
+    sample of the workload's lookups on every core of the GPU's share (at most
+    16), and median of 3 on one core.  Value rows are copied from the GPU
+    table beforehand (untimed)."""
     qf = q_np.reshape(-1, 8)
     Gf = G.reshape(-1, w.m)
     rng = np.random.default_rng(123)
-    n = 256
-    while True:
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+
+    def sample(n):
         idx = np.sort(rng.choice(qf.shape[0], n, replace=False))
         qs = qf[idx]
-        t0 = time.perf_counter()
-        nb = oracle.neighbors(qs, w.K)
-        t_nb = time.perf_counter() - t0
-        sl = torch.from_numpy(nb["slot"]).to(table.device).long()
+        _omp_threads(threads)
+        sl = torch.from_numpy(oracle.neighbors(qs, w.K)["slot"]).to(table.device).long()
         rows = table[sl.clamp(min=0)].float()
         rows[sl < 0] = 0
-        rows = rows.cpu().numpy().astype(np.float64)
         g = Gf[torch.from_numpy(idx).to(table.device)].cpu().numpy().astype(np.float64)
-        t1 = time.perf_counter()
-        oracle.forward(nb, rows)
-        oracle.grad_query(nb, rows, g)
-        oracle.grad_table_rows(nb, g)
-        t_alg = time.perf_counter() - t1
-        t = t_nb + t_alg
-        if t >= 0.5 * target_s or n >= qf.shape[0]:
-            break
-        n = int(min(qf.shape[0], max(2 * n, n * target_s / max(t, 1e-3))))
-    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    # the enumeration runs on `cores` OpenMP threads; numpy's einsum, unique and
-    # add.at run on one thread
-    return {"value": n / t, "unit": "lookups/s (fwd+bwd)", "cores": cores, "kind": "oracle", "cpu": cpu_model(),
-            "threads": {"neighbour_enumeration": cores, "fp64_algebra": 1},
-            "sample": "%d random lookups of the %s batch (%.1f s: neighbour enumeration %.1f s in C on %d OpenMP "
-                      "threads, fp64 gather/grad algebra %.1f s in single-threaded numpy; rows copied from the GPU "
-                      "table untimed)" % (n, w.name, t, t_nb, cores, t_alg)}
+        return qs, rows.cpu().numpy(), g
+
+    def timed(n, nthreads, budget):
+        """Median of 3 passes; the sample grows until one pass takes ~budget s."""
+        while True:
+            qs, rows, g = sample(n)
+            t = _oracle_pass(oracle, qs, rows, g, w.K, nthreads)
+            if t >= 0.5 * budget or n >= qf.shape[0]:
+                break
+            n = int(min(qf.shape[0], max(2 * n, n * budget / max(t, 1e-3))))
+        ts = sorted([t] + [_oracle_pass(oracle, qs, rows, g, w.K, nthreads) for _ in range(2)])
+        return n, ts
+
+    n_all, t_all = timed(4096, threads, target_s / 5)
+    n_one, t_one = timed(1024, 1, target_s / 10)
+    _omp_threads(threads)
+    return {"value": n_all / t_all[1], "unit": "lookups/s (fwd+bwd)", "cores": threads, "kind": "oracle",
+            "cpu": cpu_info(), "one_core": {"value": n_one / t_one[1], "lookups": n_one, "seconds": t_one},
+            "seconds": t_all,
+            "sample": "%d random lookups of the %s batch, median of 3 passes (%.2f / %.2f / %.2f s) on %d threads: "
+                      "neighbour enumeration in C (OpenMP), forward, dq and value gradient in numpy over lookup "
+                      "chunks, gradient rows merged per row partition; one core: %d lookups, median %.2f s; value "
+                      "rows copied from the GPU table untimed" % (
+                          n_all, w.name, t_all[0], t_all[1], t_all[2], threads, n_one, t_one[1])}
 
 
 def measured_traffic(workload: str, kernel: str):
@@ -144,7 +206,10 @@ def main():
     ap.add_argument("--mode", default="auto", choices=["auto", "atomic", "sorted", "merged"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-compare", action="store_true", help="skip timing the other scatter modes")
+    ap.add_argument("--no-compare", action="store_true",
+                    help="skip timing the other scatter modes and the step variants (no shared order, saved lists)")
+    ap.add_argument("--no-order", action="store_true",
+                    help="no shared lookup order in the timed step (the backward sorts on its own)")
     ap.add_argument("--no-theta", action="store_true", help="skip timing the activation layer path")
     ap.add_argument("--no-k", action="store_true", help="skip timing the variable-k lookups")
     ap.add_argument("--no-subnetwork", action="store_true", help="skip timing the memory subnetwork slice")
@@ -199,33 +264,97 @@ def main():
 
     stream = torch.cuda.current_stream()
     mode = lram.resolved_mode(w.B, w.H, args.mode)
-    log("value-gradient scatter: %s" % mode)
+    # the merged scatter sorts the lookups by closest lattice point anyway: the
+    # step does it once, first, and the forward and the backward both use it
+    ordered = mode == "merged" and not args.no_order
+    log("value-gradient scatter: %s%s" % (mode, ", lookups ordered once per step" if ordered else ""))
     nbytes = lram.backward_workspace_bytes(w.B, w.H, w.m, mode)
-    wsp = torch.empty(nbytes, dtype=torch.uint8, device=dev) if nbytes else None
+    wsp = torch.empty(nbytes, dtype=torch.uint8, device=dev) if nbytes and not ordered else None
+    obuf = torch.empty(lram.order_layout(w.B, w.H)[0], dtype=torch.uint8, device=dev) if ordered else None
 
-    def step():
-        lram.forward(q, table, w.K, out=out)
-        lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, mode=mode, workspace=wsp)
+    def step(ev=None):
+        if ev:
+            ev[0].record(stream)
+        if ordered:
+            lram.order(q, w.K, obuf)
+        if ev:
+            ev[1].record(stream)
+        lram.forward(q, table, w.K, out=out, order=obuf)
+        if ev:
+            ev[2].record(stream)
+        lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, mode=mode, workspace=wsp, order=obuf)
+        if ev:
+            ev[3].record(stream)
 
     for i in range(args.warmup):
         step()
         torch.cuda.synchronize()
         log("warmup %d done" % i)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for k in range(args.steps):
-        ev[k][0].record(stream)
-        lram.forward(q, table, w.K, out=out)
-        ev[k][1].record(stream)
-        lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, mode=mode, workspace=wsp)
-        ev[k][2].record(stream)
+        step(ev[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
-    fwd_ms = float(np.mean([ev[k][0].elapsed_time(ev[k][1]) for k in range(args.steps)]))
-    bwd_ms = float(np.mean([ev[k][1].elapsed_time(ev[k][2]) for k in range(args.steps)]))
+    order_t = [ev[k][0].elapsed_time(ev[k][1]) for k in range(args.steps)]
+    fwd_t = [ev[k][1].elapsed_time(ev[k][2]) for k in range(args.steps)]
+    bwd_t = [ev[k][2].elapsed_time(ev[k][3]) for k in range(args.steps)]
+    step_t = [ev[k][0].elapsed_time(ev[k][3]) for k in range(args.steps)]
+    order_ms, fwd_ms, bwd_ms = float(np.mean(order_t)), float(np.mean(fwd_t)), float(np.mean(bwd_t))
     ms_step = wall * 1e3 / args.steps
-    log("timed %d steps: %.3f ms/step (forward %.3f ms, backward %.3f ms)" % (args.steps, ms_step, fwd_ms, bwd_ms))
+    log("timed %d steps: %.3f ms/step (order %.3f ms, forward %.3f ms, backward %.3f ms; median step %.3f ms)" % (
+        args.steps, ms_step, order_ms, fwd_ms, bwd_ms, float(np.median(step_t))))
+    timing = {"events_ms": {"order": {"mean": order_ms, "median": float(np.median(order_t))},
+                            "forward": {"mean": fwd_ms, "median": float(np.median(fwd_t))},
+                            "backward": {"mean": bwd_ms, "median": float(np.median(bwd_t))},
+                            "step": {"mean": float(np.mean(step_t)), "median": float(np.median(step_t)),
+                                     "min": float(np.min(step_t)), "max": float(np.max(step_t))}},
+              "protocol": "%d warm-up steps, then %d timed steps back to back; HIP events on the launch stream "
+                          "around each call; value and ms_per_step from the host clock around all %d" % (
+                              args.warmup, args.steps, args.steps)}
+
+    # the same step without the shared order (the backward sorts on its own),
+    # and with the saved neighbour lists (the backward skips its search): not
+    # part of `value`
+    variants = {}
+    if not args.no_compare:
+        def timed_pair(f_fwd, f_bwd, reps=5):
+            f_fwd()
+            f_bwd()
+            torch.cuda.synchronize()
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            tf = tb = 0.0
+            for _ in range(reps):
+                e[0].record(stream)
+                f_fwd()
+                e[1].record(stream)
+                f_bwd()
+                e[2].record(stream)
+                torch.cuda.synchronize()
+                tf += e[0].elapsed_time(e[1]) / reps
+                tb += e[1].elapsed_time(e[2]) / reps
+            return tf, tb
+
+        if ordered:
+            nws = lram.backward_workspace_bytes(w.B, w.H, w.m, mode)
+            wsu = torch.empty(nws, dtype=torch.uint8, device=dev)
+            tf, tb = timed_pair(lambda: lram.forward(q, table, w.K, out=out),
+                                lambda: lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, mode=mode,
+                                                      workspace=wsu))
+            variants["unordered"] = {"fwd_ms": tf, "bwd_ms": tb, "step_ms": tf + tb,
+                                     "what": "forward in lookup order; the backward sorts by closest point itself"}
+            log("without the shared order: forward %.3f ms, backward %.3f ms" % (tf, tb))
+            del wsu
+        nl = lram.new_lists(q)
+        tf, tb = timed_pair(lambda: lram.forward(q, table, w.K, out=out, order=obuf, lists=nl),
+                            lambda: lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, mode=mode,
+                                                  workspace=wsp, order=obuf, lists=nl))
+        variants["saved_lists"] = {"fwd_ms": tf, "bwd_ms": tb, "step_ms": tf + tb + order_ms,
+                                   "what": "the forward also writes the 32 (location, weight, code) entries of "
+                                           "every lookup (384 B); the backward reads them instead of searching"}
+        log("with saved neighbour lists: forward %.3f ms, backward %.3f ms" % (tf, tb))
+        del nl
     # what the accumulate-into contract spares every step: clearing the whole
     # gradient table (outside the timed steps, not part of `value`)
     ez = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
@@ -237,7 +366,9 @@ def main():
     log("clearing the %.1f GB gradient table: %.2f ms" % (gtab.numel() * 4 / 1e9, zero_ms))
 
     # the other value-gradient scatters, timed the same way for comparison (not part of `value`)
-    by_scatter = {mode: bwd_ms}
+    # backward calls as a caller without an order makes them (the merged one
+    # sorting on its own); sorted is the bit-reproducible scatter
+    by_scatter = {mode: variants["unordered"]["bwd_ms"] if "unordered" in variants else bwd_ms}
     del wsp
     for other in ("atomic", "sorted", "merged"):
         if other == mode or args.no_compare:
@@ -325,8 +456,11 @@ def main():
     fwd_req = L * (32 + w.m * st + 32 * w.m * st)
     bwd_req = L * (32 + w.m * 4 + 32 + 32 * (w.m * st + 2 * w.m * 4))
     if bwd_ms >= fwd_ms:
-        # the atomic backward is one kernel; the other modes time their whole
-        # pass (lookup/location sort + fused kernel) between the same events
+        # the atomic backward is one kernel; the other modes time every kernel
+        # of the call between the same events (merged: the gated atomic kernel
+        # and the fused kernel, plus the cell keys and the lookup sort when no
+        # order is shared; sorted: the fused kernel, the pair sort and the
+        # segmented reduction)
         kname = {"atomic": "k_backward_atomic", "merged": "backward_pass_merged",
                  "sorted": "backward_pass_sorted"}[mode]
         kms, kbytes, kreq = bwd_ms, bwd_bytes, bwd_req
@@ -351,10 +485,14 @@ def main():
         "dtype": "f32",  # the path's arithmetic; the table's storage type is config.table_dtype
         "data": "synthetic (seeded; see workloads.py)",
         "config": {"workload": w.name, "K": list(w.K), "locations": w.N, "m": w.m, "table_dtype": w.dtype,
-                   "batch": w.B, "heads": w.H, "lookups": L, "scatter": mode, "parallelism": "none (1 GPU)"},
+                   "batch": w.B, "heads": w.H, "lookups": L, "scatter": mode, "ordered": ordered,
+                   "parallelism": "none (1 GPU)"},
         "fwd_lookups_per_s": L / (fwd_ms * 1e-3),
+        "order_ms": order_ms,
         "fwd_ms": fwd_ms,
         "bwd_ms": bwd_ms,
+        "timing": timing,
+        "variants": variants,
         "bwd_ms_by_scatter": by_scatter,
         "distinct_rows": U,
         "grad_table_zero_ms": zero_ms,
@@ -478,9 +616,15 @@ def time_small_graph(torch, lram, W, log, reps=200):
         nws = lram.backward_workspace_bytes(w.B, w.H, w.m, mode)
         ws = torch.empty(nws, dtype=torch.uint8, device="cuda") if nws else None
 
+        nl = lram.new_lists(q)
+
         def step():
             lram.forward(q, table, w.K, out=o)
             lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, mode=mode, workspace=ws)
+
+        def step_saved():
+            lram.forward(q, table, w.K, out=o, lists=nl)
+            lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq, mode=mode, workspace=ws, lists=nl)
 
         def timed(f):
             for _ in range(10):
@@ -494,21 +638,44 @@ def time_small_graph(torch, lram, W, log, reps=200):
             torch.cuda.synchronize()
             return e0.elapsed_time(e1) / reps * 1e3
 
+        def captured(f):
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                f()
+            torch.cuda.current_stream().wait_stream(side)
+            torch.cuda.synchronize()
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                f()
+            return graph
+
+        def kernel_us(f):
+            """Kernel time of one step: HIP events around each of `reps` steps
+            with the host waiting in between (no launch overlap)."""
+            ts = []
+            for _ in range(20):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                f()
+                e1.record()
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1) * 1e3)
+            return float(np.median(ts))
+
         eager_us = timed(step)
-        side = torch.cuda.Stream()
-        side.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(side):
-            step()
-        torch.cuda.current_stream().wait_stream(side)
-        torch.cuda.synchronize()
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            step()
+        graph = captured(step)
         graph_us = timed(graph.replay)
+        eager_saved_us = timed(step_saved)
+        graph_s = captured(step_saved)
+        graph_saved_us = timed(graph_s.replay)
         out[name] = {"lookups": w.L, "scatter": mode, "eager_us": eager_us, "graph_us": graph_us,
-                     "graph_lookups_per_s": w.L / (graph_us * 1e-6)}
-        log("%s: fwd+bwd step %.1f us eager, %.1f us graph replay" % (name, eager_us, graph_us))
-        del graph, q, table, G, gtab, o, gq, ws
+                     "graph_lookups_per_s": w.L / (graph_us * 1e-6),
+                     "saved_lists": {"eager_us": eager_saved_us, "graph_us": graph_saved_us},
+                     "isolated_step_us": {"recompute": kernel_us(step), "saved_lists": kernel_us(step_saved)}}
+        log("%s: fwd+bwd step %.1f us eager, %.1f us graph replay; with saved lists %.1f / %.1f us" % (
+            name, eager_us, graph_us, eager_saved_us, graph_saved_us))
+        del graph, graph_s, q, table, G, gtab, o, gq, ws, nl
         torch.cuda.empty_cache()
     return out
 

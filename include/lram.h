@@ -61,7 +61,8 @@ extern "C" {
 
 typedef enum {
   LRAM_OK = 0,
-  LRAM_EINVAL = 1,      /* null pointer with L > 0, negative size, L >= 2^31, misaligned pointer */
+  LRAM_EINVAL = 1,      /* null pointer with L > 0, negative size, L >= 2^31, misaligned pointer,
+                           undersized order buffer, saved lists incomplete */
   LRAM_EBADK = 2,       /* a K_i odd, < 2 or > 8192, N != prod K, or N >= 2^31 */
   LRAM_EDTYPE = 3,      /* unknown dtype or unsupported m for that dtype */
   LRAM_EWORKSPACE = 4,  /* workspace missing or smaller than lram_backward_workspace_bytes */
@@ -73,7 +74,8 @@ typedef enum { LRAM_F32 = 0, LRAM_BF16 = 1 } lram_dtype;
 
 typedef enum {
   LRAM_SCATTER_ATOMIC = 0, /* fp32 atomic adds straight into grad_table */
-  LRAM_SCATTER_SORTED = 1, /* sort (slot, lookup) pairs, one read-modify-write per touched row */
+  LRAM_SCATTER_SORTED = 1, /* sort (slot, lookup) pairs, one read-modify-write per touched row;
+                              bit-reproducible from call to call */
   LRAM_SCATTER_MERGED = 2, /* order lookups by their closest lattice point, merge equal slots within
                               each batch of consecutive lookups (64 for lists of up to 32, 32 for
                               longer ones), one atomic row per distinct slot;
@@ -82,7 +84,7 @@ typedef enum {
   LRAM_SCATTER_AUTO = 3    /* MERGED for L >= 131072 lookups, ATOMIC below (the sort does not pay off) */
 } lram_scatter_mode;
 
-/* Library version (major*10000 + minor*100 + patch). */
+/* Library version (major*10000 + minor*100 + patch): 200 = 0.2.0. */
 int lram_version(void);
 
 /* Static description of a status code. */
@@ -104,17 +106,65 @@ int lram_neighbors(const float* q, int64_t B, int64_t H, const int32_t K[8], int
                    float* d2, void* stream);
 
 /*
+ * Lookup order (Sec. 2.6: lookups whose queries share their closest lattice
+ * point share most of their 32 neighbours).
+ *
+ * lram_order_bytes -- size of an order buffer for L = B*H lookups (host only),
+ * and the byte offsets of its two documented arrays (nullable outputs).
+ *
+ * lram_order -- fills `order` (device, 256-byte aligned, at least
+ * lram_order_bytes) for the queries q: the lookups sorted, stably, by the
+ * location of their closest lattice point (the first point of Sec. 2.6's
+ * reduction; where several points are equally close in exact arithmetic, one
+ * of them -- not necessarily the one the fp32 distance recipe lists first):
+ *   bytes [0, 4)            uint32: how many lookups share their key with a
+ *                           neighbour in the order (decides, on the device,
+ *                           whether the merged scatter merges)
+ *   keys  [L] uint32        at keys_offset: the sorted keys (location, or N for a
+ *                           non-finite query)
+ *   perm  [L] uint32        at perm_offset: the lookup at each position
+ *   the rest                scratch of the sort.
+ * The same buffer serves as the merged scatter's workspace.  An order may be
+ * passed to lram_forward and lram_backward of the same q, B, H and K: both then
+ * visit the lookups in this order (workgroups take consecutive positions, each
+ * XCD one contiguous range, so lookups that read the same rows run on the
+ * same L2), and the merged scatter uses it instead of sorting again.  An order
+ * written for other queries gives wrong results but never addresses outside
+ * the caller's buffers (positions outside [0, L) are skipped).
+ */
+int lram_order_bytes(int64_t B, int64_t H, size_t* bytes, size_t* keys_offset, size_t* perm_offset);
+int lram_order(const float* q, int64_t B, int64_t H, const int32_t K[8], void* order, size_t order_bytes,
+               void* stream);
+
+/*
  * lram_forward -- out[l][:] = sum_j w_j table[slot_j][:] (Sec. 2.2 with the
  * truncation of Sec. 2.6), fp32 accumulation, written once in the table dtype
  * (bf16: round to nearest even).  table holds N rows of m elements.
+ *   order/order_bytes  nullable: an order from lram_order for these queries
+ *                      (the lookups are then visited in that order; out is the
+ *                      same).
+ *   nbr_slot [L][32] int32, nbr_w [L][32] fp32, nbr_code [L][32] uint32:
+ *                      nullable (all three or none): the neighbour lists saved
+ *                      for lram_backward (Sec. 2.6: the kernel hands the
+ *                      indices alpha_i and the weights w_i to the autograd
+ *                      wrapper).  Entry j of lookup l: the location (-1 for
+ *                      padding), the recipe weight, and the point's coordinates
+ *                      p in its query's fundamental-region frame (Sec. 2.6:
+ *                      the point is c + sigma pi^-1 p for the query's closest
+ *                      point c and signed permutation sigma pi), eight 3-bit
+ *                      fields p_r + 3 in bits [3r, 3r + 3), 0 for padding.  The
+ *                      32 entries are those of lram_neighbors in the search's
+ *                      own order (padding last).  384 bytes per lookup.
  */
 int lram_forward(const float* q, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
-                 int64_t N, int32_t m, void* out, void* stream);
+                 int64_t N, int32_t m, void* out, const void* order, size_t order_bytes, int32_t* nbr_slot,
+                 float* nbr_w, uint32_t* nbr_code, void* stream);
 
 /*
  * lram_backward_workspace_bytes -- device workspace needed by lram_backward
  * (and lram_backward_k, lram_theta_backward) for L = B*H lookups in the given
- * scatter mode (0 for LRAM_SCATTER_ATOMIC; the same for every k).
+ * scatter mode (0 for LRAM_SCATTER_ATOMIC; the same for every k; the merged
+ * scatter's workspace is an order buffer, lram_order_bytes).
  */
 int lram_backward_workspace_bytes(int64_t B, int64_t H, int32_t m, int mode, size_t* bytes);
 
@@ -136,16 +186,30 @@ int lram_scatter_mode_resolved(int64_t B, int64_t H, int mode, int* resolved);
  *        under LRAM_SCATTER_SORTED)
  *   grad_q[l][i] = sum_j -2 u_j^3 (x_i - k_{j,i}) <grad_out[l], table[slot_j]>,
  *       u_j = 1 - s_j/8 (overwritten; nullable to skip it)
- * The neighbour search is recomputed from q.  workspace/ws_bytes: device
- * buffer, 256-byte aligned, of at least lram_backward_workspace_bytes (may be
- * NULL for the atomic mode); its contents on entry do not matter, and calls
- * that may overlap need workspaces of their own.  The sorted
- * mode needs 32 L < 2^32.  grad_table may be NULL only if grad_q is not
- * (without grad_table every mode computes grad_q the same way).
+ * order/order_bytes: nullable; an order from lram_order for these queries.
+ * The merged scatter then takes it instead of sorting (no workspace needed),
+ * the atomic one visits the lookups in it, the sorted one ignores it.
+ * nbr_slot/nbr_w/nbr_code: nullable (all three or none); the lists lram_forward
+ * saved for these queries replace the neighbour search (each entry's distance
+ * is recomputed from its code for dq).  Entries whose location is outside
+ * [0, N) count as padding, so lists of other queries give wrong gradients but
+ * never address outside grad_table.  Without them the search is recomputed
+ * from q.
+ * workspace/ws_bytes: device buffer, 256-byte aligned, of at least
+ * lram_backward_workspace_bytes (may be NULL for the atomic mode, and for the
+ * merged mode when an order is given); its contents on entry do not matter,
+ * and calls that may overlap need workspaces of their own.
+ * LRAM_SCATTER_SORTED is bit-reproducible: the same inputs give the same
+ * grad_table bits on every call (every row's sum is formed in one fixed
+ * order, each row written by one thread group); it needs 32 L < 2^32.  The
+ * atomic and merged modes add in an order that varies from call to call.
+ * grad_table may be NULL only if grad_q is not (without grad_table every mode
+ * computes grad_q the same way, bit for bit).
  */
 int lram_backward(const float* q, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
-                  int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_q, int mode,
-                  void* workspace, size_t ws_bytes, void* stream);
+                  int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_q, const void* order,
+                  size_t order_bytes, const int32_t* nbr_slot, const float* nbr_w, const uint32_t* nbr_code,
+                  int mode, void* workspace, size_t ws_bytes, void* stream);
 
 /*
  * Training-side companions.

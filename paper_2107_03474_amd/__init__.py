@@ -15,7 +15,7 @@ from __future__ import annotations
 import ctypes
 import os
 import threading
-from typing import Optional, Sequence, Tuple
+from typing import NamedTuple, Optional, Sequence, Tuple
 
 import numpy as np
 import torch  # noqa: F401  -- loads the HIP runtime liblram.so must share
@@ -24,7 +24,8 @@ __all__ = ["neighbors", "forward", "backward", "backward_workspace_bytes", "look
            "library_path", "load", "LramError", "F32", "BF16", "SCATTER_ATOMIC", "SCATTER_SORTED",
            "SCATTER_MERGED", "SCATTER_AUTO", "resolved_mode", "NB",
            "theta_coords", "theta_forward", "theta_backward", "ThetaLookup", "theta", "ALL", "MAX_SUPPORT",
-           "list_width", "access_histogram", "access_stats", "sparse_adam", "SparseAdam"]
+           "list_width", "access_histogram", "access_stats", "sparse_adam", "SparseAdam", "Lists", "new_lists",
+           "order", "order_layout", "order_view"]
 
 NB = 32
 F32, BF16 = 0, 1
@@ -61,13 +62,19 @@ def load():
             lib.lram_last_hip_error.restype = I
             lib.lram_neighbors.argtypes = [P, I64, I64, P, P, P, P, P]
             lib.lram_neighbors.restype = I
-            lib.lram_forward.argtypes = [P, I64, I64, P, P, I, I64, I32, P, P]
+            lib.lram_forward.argtypes = [P, I64, I64, P, P, I, I64, I32, P, P, ctypes.c_size_t, P, P, P, P]
             lib.lram_forward.restype = I
+            SZP = ctypes.POINTER(ctypes.c_size_t)
+            lib.lram_order_bytes.argtypes = [I64, I64, SZP, SZP, SZP]
+            lib.lram_order_bytes.restype = I
+            lib.lram_order.argtypes = [P, I64, I64, P, P, ctypes.c_size_t, P]
+            lib.lram_order.restype = I
             lib.lram_backward_workspace_bytes.argtypes = [I64, I64, I32, I, ctypes.POINTER(ctypes.c_size_t)]
             lib.lram_backward_workspace_bytes.restype = I
             lib.lram_scatter_mode_resolved.argtypes = [I64, I64, I, ctypes.POINTER(ctypes.c_int)]
             lib.lram_scatter_mode_resolved.restype = I
-            lib.lram_backward.argtypes = [P, I64, I64, P, P, I, I64, I32, P, P, P, I, P, ctypes.c_size_t, P]
+            lib.lram_backward.argtypes = [P, I64, I64, P, P, I, I64, I32, P, P, P, P, ctypes.c_size_t, P, P, P, I, P,
+                                          ctypes.c_size_t, P]
             lib.lram_backward.restype = I
             lib.lram_neighbors_k.argtypes = [P, I64, I64, P, I32, P, P, P, P]
             lib.lram_neighbors_k.restype = I
@@ -182,9 +189,72 @@ def neighbors(q: torch.Tensor, K: Sequence[int], want_d2: bool = True, k: int = 
     return slot, w, d2
 
 
+class Lists(NamedTuple):
+    """Neighbour lists saved by ``forward`` for ``backward`` (each [..., 32]):
+    location (-1 padding), recipe weight, and the point's code in its query's
+    fundamental-region frame."""
+    slot: torch.Tensor
+    w: torch.Tensor
+    code: torch.Tensor
+
+
+def new_lists(q: torch.Tensor) -> Lists:
+    """Uninitialised saved-list buffers for the lookups of q [..., 8]."""
+    lead = q.shape[:-1] + (NB,)
+    return Lists(torch.empty(lead, dtype=torch.int32, device=q.device),
+                 torch.empty(lead, dtype=torch.float32, device=q.device),
+                 torch.empty(lead, dtype=torch.int32, device=q.device))
+
+
+def _lists(nl: Optional[Lists], q: torch.Tensor):
+    if nl is None:
+        return None, None, None
+    lead = q.shape[:-1] + (NB,)
+    return (_dev(nl.slot, "lists.slot", torch.int32, lead, like=q), _dev(nl.w, "lists.w", torch.float32, lead, like=q),
+            _dev(nl.code, "lists.code", torch.int32, lead, like=q))
+
+
+def order_layout(B: int, H: int) -> Tuple[int, int, int]:
+    """(bytes, keys offset, perm offset) of an order buffer for B*H lookups."""
+    lib = load()
+    n, ko, po = ctypes.c_size_t(0), ctypes.c_size_t(0), ctypes.c_size_t(0)
+    _check(lib.lram_order_bytes(B, H, ctypes.byref(n), ctypes.byref(ko), ctypes.byref(po)))
+    return n.value, ko.value, po.value
+
+
+def order(q: torch.Tensor, K: Sequence[int], buf: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """The lookups of q sorted by the location of their closest lattice point
+    (lram_order): a uint8 device buffer to pass as ``order=`` to forward and
+    backward (and usable as the merged scatter's workspace)."""
+    lib = load()
+    B, H = _bh(q)
+    nbytes = order_layout(B, H)[0]
+    if buf is None:
+        buf = torch.empty(nbytes, dtype=torch.uint8, device=q.device)
+    _check(lib.lram_order(_dev(q, "q", torch.float32), B, H, _K(K), _dev(buf, "order", torch.uint8, like=q),
+                          buf.numel(), _stream(q)))
+    return buf
+
+
+def order_view(buf: torch.Tensor, L: int):
+    """(shared count [1], keys [L], perm [L]) int32 views of an order buffer
+    (uint32 values; L < 2^31 keeps them non-negative)."""
+    _, ko, po = order_layout(L, 1)
+    w = buf.view(torch.int32)
+    return w[:1], w[ko // 4:ko // 4 + L], w[po // 4:po // 4 + L]
+
+
+def _order(buf: Optional[torch.Tensor], q: torch.Tensor):
+    if buf is None:
+        return None, 0
+    return _dev(buf, "order", torch.uint8, like=q), buf.numel()
+
+
 def forward(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], out: Optional[torch.Tensor] = None,
-            k: int = NB):
-    """phi(q) over the closest k points (k = ALL: the whole support): [..., m] in the table dtype."""
+            k: int = NB, order: Optional[torch.Tensor] = None, lists: Optional[Lists] = None):
+    """phi(q) over the closest k points (k = ALL: the whole support): [..., m] in the table dtype.
+    k = 32 only: ``order`` (from ``order()``) visits the lookups in that order;
+    ``lists`` (from ``new_lists``) receives the neighbour lists for ``backward``."""
     lib = load()
     B, H = _bh(q)
     N, m = _table_shape(table)
@@ -193,8 +263,10 @@ def forward(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], out: Optiona
     args = (_dev(q, "q", torch.float32), B, H, _K(K), _dev(table, "table", like=q), _table_dtype(table), N, m)
     o = _dev(out, "out", table.dtype, q.shape[:-1] + (m,), like=q)
     if k == NB:
-        _check(lib.lram_forward(*args, o, _stream(q)))
+        _check(lib.lram_forward(*args, o, *_order(order, q), *_lists(lists, q), _stream(q)))
     else:
+        if order is not None or lists is not None:
+            raise LramError("order and saved lists are offered for k = 32 only")
         _check(lib.lram_forward_k(*args, int(k), o, _stream(q)))
     return out
 
@@ -216,11 +288,14 @@ def backward_workspace_bytes(B: int, H: int, m: int, mode="auto") -> int:
 
 def backward(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], grad_out: torch.Tensor,
              grad_table: Optional[torch.Tensor] = None, want_grad_q: bool = True, mode="auto",
-             workspace: Optional[torch.Tensor] = None, grad_q: Optional[torch.Tensor] = None, k: int = NB):
+             workspace: Optional[torch.Tensor] = None, grad_q: Optional[torch.Tensor] = None, k: int = NB,
+             order: Optional[torch.Tensor] = None, lists: Optional[Lists] = None):
     """Gradients: grad_table [N, m] fp32 is ACCUMULATED into (allocated zeroed if None,
     pass False to skip), grad_q [..., 8] fp32 (None unless want_grad_q; written into
     ``grad_q`` when given).  k != 32 (variable k / ALL) takes the atomic and
-    merged scatters (and "auto"), not the sorted one."""
+    merged scatters (and "auto"), not the sorted one.  k = 32 only: ``order``
+    (from ``order()``) replaces the merged scatter's sort; ``lists`` (filled by
+    ``forward``) replace the neighbour search."""
     lib = load()
     B, H = _bh(q)
     N, m = _table_shape(table)
@@ -235,37 +310,46 @@ def backward(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], grad_out: t
              _dev(gq, "grad_q", torch.float32, q.shape, like=q) if gq is not None else None)
     mode_i = _MODES[mode]
     ws_bytes = backward_workspace_bytes(B, H, m, mode_i)
-    if ws_bytes and workspace is None:
+    merged_with_order = order is not None and resolved_mode(B, H, mode_i) == "merged"
+    if ws_bytes and workspace is None and not merged_with_order:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
     if k != NB:
+        if order is not None or lists is not None:
+            raise LramError("order and saved lists are offered for k = 32 only")
         _check(lib.lram_backward_k(*head, int(k), *grads, mode_i, *_workspace(workspace, q), _stream(q)))
     else:
-        _check(lib.lram_backward(*head, *grads, mode_i, *_workspace(workspace, q), _stream(q)))
+        _check(lib.lram_backward(*head, *grads, *_order(order, q), *_lists(lists, q), mode_i,
+                                 *_workspace(workspace, q), _stream(q)))
     return (grad_table if grad_table is not False else None), gq
 
 
 class LramLookup(torch.autograd.Function):
-    """Autograd wrapper (Sec. 2.6): forward phi(q); backward gives dq and a dense dtable."""
+    """Autograd wrapper (Sec. 2.6): forward phi(q); backward gives dq and a dense
+    dtable.  save_lists: the forward keeps the neighbour lists (384 bytes per
+    lookup) and the backward reuses them instead of searching again."""
 
     @staticmethod
-    def forward(ctx, q, table, K, mode):
+    def forward(ctx, q, table, K, mode, save_lists):
         q, table = q.contiguous(), table.contiguous()
-        ctx.save_for_backward(q, table)
         ctx.K = tuple(int(k) for k in K)
         ctx.mode = mode
-        return forward(q, table, ctx.K)
+        nl = new_lists(q) if save_lists else None
+        out = forward(q, table, ctx.K, lists=nl)
+        ctx.save_for_backward(q, table, *(nl if nl is not None else ()))
+        return out
 
     @staticmethod
     def backward(ctx, g):
-        q, table = ctx.saved_tensors
+        q, table, *saved = ctx.saved_tensors
         g32 = g.contiguous().to(torch.float32)
         gt, gq = backward(q, table, ctx.K, g32, grad_table=None if ctx.needs_input_grad[1] else False,
-                          want_grad_q=ctx.needs_input_grad[0], mode=ctx.mode)
-        return gq, (gt.to(table.dtype) if gt is not None else None), None, None
+                          want_grad_q=ctx.needs_input_grad[0], mode=ctx.mode,
+                          lists=Lists(*saved) if saved else None)
+        return gq, (gt.to(table.dtype) if gt is not None else None), None, None, None
 
 
-def lookup(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], mode="auto") -> torch.Tensor:
-    return LramLookup.apply(q, table, tuple(K), mode)
+def lookup(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], mode="auto", save_lists: bool = False) -> torch.Tensor:
+    return LramLookup.apply(q, table, tuple(K), mode, bool(save_lists))
 
 
 # ---------------------------------------------------------------------------

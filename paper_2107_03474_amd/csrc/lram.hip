@@ -119,22 +119,21 @@ int dispatch(int dtype, int32_t m, Args... args) {
 
 template <int DT, int M>
 struct FwdLaunch {
-  static int go(const float* q, const Params& P, const void* table, void* out, bool th, hipStream_t s) {
+  static int go(const float* q, const Params& P, const void* table, void* out, bool th, const uint32_t* perm,
+                NbrList save, hipStream_t s) {
+    const dim3 g(grid_for(P)), b(THREADS);
     if (th)
-      hipLaunchKernelGGL((k_forward<DT, M, true>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, out);
+      hipLaunchKernelGGL((k_forward<DT, M, true>), g, b, 0, s, q, P, table, out, perm, save);
+    else if (perm && save.on())
+      hipLaunchKernelGGL((k_forward<DT, M, false, true, true>), g, b, 0, s, q, P, table, out, perm, save);
+    else if (perm)
+      hipLaunchKernelGGL((k_forward<DT, M, false, true, false>), g, b, 0, s, q, P, table, out, perm, save);
+    else if (save.on())
+      hipLaunchKernelGGL((k_forward<DT, M, false, false, true>), g, b, 0, s, q, P, table, out, perm, save);
     else
-      hipLaunchKernelGGL((k_forward<DT, M, false>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, out);
+      hipLaunchKernelGGL((k_forward<DT, M, false>), g, b, 0, s, q, P, table, out, perm, save);
     return launched();
   }
-};
-
-// Radix-sort buffers for n (key, value) pairs.
-struct SortWs {
-  uint32_t *k0, *k1, *hist, *totals;
-  uint2 *v0, *v1;
-  int64_t n;
-  int nblocks;
-  int64_t nh, nbt;
 };
 
 size_t align256(size_t b) { return (b + 255) & ~size_t(255); }
@@ -151,110 +150,228 @@ struct Carver {
   }
 };
 
-void carve_sort(int64_t n, Carver& c, SortWs* ws) {
+// Radix-sort buffers for n keys with payloads of type V, ping-ponged between
+// (ka, va) and (kb, vb).
+template <typename V>
+struct Radix {
+  uint32_t *ka, *kb;
+  V *va, *vb;
+  uint32_t *hist, *totals;
+  int64_t n;
+  int nblocks;
+  int64_t nh, nbt;
+};
+
+template <typename V>
+void carve_radix_scratch(int64_t n, Carver& c, Radix<V>* r) {
   const int nblocks = (int)((n + SORT_TILE - 1) / SORT_TILE);
   const int64_t nh = (int64_t)RADIX * nblocks;
   const int64_t nbt = (nh + SCAN_TILE - 1) / SCAN_TILE;
-  char* k0 = c.take(n * 4);
-  char* k1 = c.take(n * 4);
-  char* v0 = c.take(n * 8);
-  char* v1 = c.take(n * 8);
   char* h = c.take(nh * 4);
   char* tt = c.take(nbt * 4);
-  if (ws) {
-    ws->k0 = (uint32_t*)k0; ws->k1 = (uint32_t*)k1; ws->v0 = (uint2*)v0; ws->v1 = (uint2*)v1;
-    ws->hist = (uint32_t*)h; ws->totals = (uint32_t*)tt;
-    ws->n = n; ws->nblocks = nblocks; ws->nh = nh; ws->nbt = nbt;
+  if (r) {
+    r->hist = (uint32_t*)h;
+    r->totals = (uint32_t*)tt;
+    r->n = n;
+    r->nblocks = nblocks;
+    r->nh = nh;
+    r->nbt = nbt;
   }
 }
 
-// Workspace of the sorted scatter: the sort of the 32 L (location, position) pairs.
-size_t sort_ws_layout(int64_t L, SortWs* ws, char* base) {
-  Carver c{base};
-  carve_sort(L * NB, c, ws);
-  return c.off;
-}
-
-// Workspace of the batch-merged scatter: the sort of the L lookups by the
-// location of their closest lattice point, and the merge gate's counter.
-struct MergeWs {
-  SortWs sort;
-  uint32_t* shared;  // lookups sharing their closest lattice point (the merge gate)
-};
-
-size_t merge_ws_layout(int64_t L, MergeWs* ws, char* base) {
-  Carver c{base};
-  carve_sort(L, c, ws ? &ws->sort : nullptr);
-  char* sh = c.take(4);
-  if (ws) ws->shared = (uint32_t*)sh;
-  return c.off;
-}
-
-// Stable LSD radix sort of (key, value) pairs with keys in [0, N]; returns the
-// buffers holding the result.
-int radix_sort(const SortWs& ws, uint32_t N, hipStream_t s, uint32_t** kres, uint2** vres) {
+int radix_passes(uint32_t N) {
   int bits = 0;
   while (bits < 32 && (N >> bits) != 0) ++bits;
-  uint32_t* kin = ws.k0;
-  uint32_t* kout = ws.k1;
-  uint2* vin = ws.v0;
-  uint2* vout = ws.v1;
-  for (int shift = 0; shift < bits; shift += RADIX_BITS) {
-    hipLaunchKernelGGL(k_radix_hist, dim3(ws.nblocks), dim3(THREADS), 0, s, kin, ws.n, shift, ws.hist, ws.nblocks);
-    hipLaunchKernelGGL(k_scan_blocks, dim3((unsigned)ws.nbt), dim3(THREADS), 0, s, ws.hist, ws.nh, ws.totals);
-    hipLaunchKernelGGL(k_scan_totals, dim3(1), dim3(THREADS), 0, s, ws.totals, ws.nbt);
-    hipLaunchKernelGGL(k_scan_add, dim3((unsigned)ws.nbt), dim3(THREADS), 0, s, ws.hist, ws.nh, ws.totals);
-    hipLaunchKernelGGL(k_radix_scatter, dim3(ws.nblocks), dim3(THREADS), 0, s, kin, vin, ws.n, shift, ws.hist,
-                       ws.nblocks, kout, vout);
+  return (bits + RADIX_BITS - 1) / RADIX_BITS;
+}
+
+// Stable LSD radix sort of the n (key, payload) pairs in (ka, va), keys in
+// [0, N]: the result is in (ka, va) after an even number of passes and in
+// (kb, vb) after an odd one.  IDENT: the payload of element i is i (va is
+// not read).
+template <typename V, bool IDENT>
+int radix_sort(const Radix<V>& r, uint32_t N, hipStream_t s) {
+  uint32_t* kin = r.ka;
+  uint32_t* kout = r.kb;
+  V* vin = r.va;
+  V* vout = r.vb;
+  const int passes = radix_passes(N);
+  for (int p = 0; p < passes; ++p) {
+    const int shift = p * RADIX_BITS;
+    hipLaunchKernelGGL(k_radix_hist, dim3(r.nblocks), dim3(THREADS), 0, s, kin, r.n, shift, r.hist, r.nblocks);
+    hipLaunchKernelGGL(k_scan_blocks, dim3((unsigned)r.nbt), dim3(THREADS), 0, s, r.hist, r.nh, r.totals);
+    hipLaunchKernelGGL(k_scan_totals, dim3(1), dim3(THREADS), 0, s, r.totals, r.nbt);
+    hipLaunchKernelGGL(k_scan_add, dim3((unsigned)r.nbt), dim3(THREADS), 0, s, r.hist, r.nh, r.totals);
+    if constexpr (IDENT) {
+      if (p == 0)
+        hipLaunchKernelGGL((k_radix_scatter<V, true>), dim3(r.nblocks), dim3(THREADS), 0, s, kin, vin, r.n, shift,
+                           r.hist, r.nblocks, kout, vout);
+      else
+        hipLaunchKernelGGL((k_radix_scatter<V, false>), dim3(r.nblocks), dim3(THREADS), 0, s, kin, vin, r.n, shift,
+                           r.hist, r.nblocks, kout, vout);
+    } else {
+      hipLaunchKernelGGL((k_radix_scatter<V, false>), dim3(r.nblocks), dim3(THREADS), 0, s, kin, vin, r.n, shift,
+                         r.hist, r.nblocks, kout, vout);
+    }
     if (int rc = launched()) return rc;
     std::swap(kin, kout);
     std::swap(vin, vout);
   }
-  *kres = kin;
-  *vres = vin;
   return LRAM_OK;
+}
+
+// The lookup order of lram_order, which is also the merged scatter's
+// workspace: a 256-byte header (word 0: the merge gate's count of lookups that
+// share their closest lattice point with a neighbour in the order), then the
+// sorted keys [L] and positions [L] (sort.ka, sort.va: the documented
+// offsets), then the sort's scratch.
+struct OrderWs {
+  uint32_t* shared;
+  Radix<uint32_t> sort;
+};
+
+constexpr size_t ORDER_KEYS_OFFSET = 256;
+
+size_t order_layout(int64_t L, OrderWs* o, char* base) {
+  Carver c{base};
+  char* hdr = c.take(ORDER_KEYS_OFFSET);
+  char* ka = c.take(L * 4);
+  char* va = c.take(L * 4);
+  char* kb = c.take(L * 4);
+  char* vb = c.take(L * 4);
+  carve_radix_scratch<uint32_t>(L, c, o ? &o->sort : nullptr);
+  if (o) {
+    o->shared = (uint32_t*)hdr;
+    o->sort.ka = (uint32_t*)ka;
+    o->sort.va = (uint32_t*)va;
+    o->sort.kb = (uint32_t*)kb;
+    o->sort.vb = (uint32_t*)vb;
+  }
+  return c.off;
+}
+
+// Workspace of the sorted scatter: the sort of the 32 L (location, (lookup, w))
+// pairs, and the segmented reduction's edge rows [groups][2][m] and flags.
+struct SortedWs {
+  Radix<uint2> sort;
+  float* edge;
+  uint32_t* flags;
+  int span;
+  int64_t groups;
+};
+
+// Pairs per group of the segmented reduction: 256, fewer when that would leave
+// CUs idle (about 32 groups per CU for 256 CUs).
+int seg_span(int64_t n) {
+  int64_t span = (n + 256 * 32 - 1) / (256 * 32);
+  return (int)(span < SEG_BATCH ? SEG_BATCH : (span > SEG_SPAN ? SEG_SPAN : span));
+}
+
+size_t sorted_layout(int64_t L, int32_t m, SortedWs* ws, char* base) {
+  Carver c{base};
+  const int64_t n = L * NB;
+  char* ka = c.take(n * 4);
+  char* kb = c.take(n * 4);
+  char* va = c.take(n * 8);
+  char* vb = c.take(n * 8);
+  carve_radix_scratch<uint2>(n, c, ws ? &ws->sort : nullptr);
+  const int span = seg_span(n);
+  const int64_t groups = (n + span - 1) / span;
+  char* edge = c.take((size_t)groups * 2 * m * 4);
+  char* flags = c.take((size_t)groups * 4);
+  if (ws) {
+    ws->sort.ka = (uint32_t*)ka;
+    ws->sort.kb = (uint32_t*)kb;
+    ws->sort.va = (uint2*)va;
+    ws->sort.vb = (uint2*)vb;
+    ws->edge = (float*)edge;
+    ws->flags = (uint32_t*)flags;
+    ws->span = span;
+    ws->groups = groups;
+  }
+  return c.off;
+}
+
+// Fills an order: closest-point keys, the stable sort (its result lands in
+// sort.ka / sort.va whatever the number of passes), and the merge gate's count.
+template <bool TH>
+int build_order(const float* q, const Params& P, const OrderWs& o, hipStream_t s) {
+  Radix<uint32_t> r = o.sort;
+  if (radix_passes(P.N) & 1) {  // start from the other buffers so the result lands in ka / va
+    std::swap(r.ka, r.kb);
+    std::swap(r.va, r.vb);
+  }
+  const dim3 kgrid((unsigned)((P.L + THREADS - 1) / THREADS));
+  hipLaunchKernelGGL(k_cell_key<TH>, kgrid, dim3(THREADS), 0, s, q, P, r.ka);
+  if (int rc = launched()) return rc;
+  if (int rc = radix_sort<uint32_t, true>(r, P.N, s)) return rc;
+  hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(WAVE), 0, s, o.shared, 0u);
+  const int64_t cb = (P.L + THREADS - 1) / THREADS;
+  hipLaunchKernelGGL(k_count_shared, dim3((unsigned)(cb < 512 ? cb : 512)), dim3(THREADS), 0, s,
+                     (const uint32_t*)o.sort.ka, P.L, o.shared);
+  return launched();
 }
 
 // q is the lookups' input: q [L][8], or z [L][16] when TH (activation layer).
 // The atomic backward kernel for lists of KS; gate is the merged scatter's
-// device-side choice (null: always scatter).
+// device-side choice (null: always scatter); perm an order to visit the
+// lookups in (null: index order); saved the forward's lists (or off).
 template <int DT, int M, bool TH, int KS>
 void launch_atomic(const float* q, const Params& P, const void* table, const float* g, float* gt, float* gq,
-                   const uint32_t* gate, hipStream_t s) {
-  hipLaunchKernelGGL((k_backward<DT, M, false, TH, KS>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g,
-                     gt, gq, (uint32_t*)nullptr, (uint2*)nullptr, gate);
+                   const uint32_t* gate, const uint32_t* perm, NbrList saved, hipStream_t s) {
+  const dim3 grid(grid_for(P)), b(THREADS);
+  uint32_t* const nk = nullptr;
+  uint2* const nv = nullptr;
+  if constexpr (!TH && KS == NB) {
+    if (perm && saved.on())
+      hipLaunchKernelGGL((k_backward<DT, M, false, false, NB, true, true>), grid, b, 0, s, q, P, table, g, gt, gq, nk,
+                         nv, gate, perm, saved);
+    else if (perm)
+      hipLaunchKernelGGL((k_backward<DT, M, false, false, NB, true, false>), grid, b, 0, s, q, P, table, g, gt, gq,
+                         nk, nv, gate, perm, saved);
+    else if (saved.on())
+      hipLaunchKernelGGL((k_backward<DT, M, false, false, NB, false, true>), grid, b, 0, s, q, P, table, g, gt, gq,
+                         nk, nv, gate, perm, saved);
+    else
+      hipLaunchKernelGGL((k_backward<DT, M, false, false, NB>), grid, b, 0, s, q, P, table, g, gt, gq, nk, nv, gate,
+                         perm, saved);
+  } else {
+    hipLaunchKernelGGL((k_backward<DT, M, false, TH, KS>), grid, b, 0, s, q, P, table, g, gt, gq, nk, nv, gate,
+                       perm, saved);
+  }
 }
 
-// The merged scatter for lists of KS: cell keys, the lookup sort and the
-// gate's count, then both the atomic kernel and the merged kernel -- the count
-// decides on the device which one works (thinly spread queries have nothing
-// to merge and keep the atomic kernel's occupancy).
+// The merged scatter for lists of KS: the lookup order (unless the caller
+// passed one: have_order), then both the atomic kernel and the merged kernel --
+// the gate's count decides on the device which one works (thinly spread
+// queries have nothing to merge and keep the atomic kernel's occupancy).
 template <int DT, int M, bool TH, int KS>
 int merged_pass(const float* q, const Params& P, const void* table, const float* g, float* gt, float* gq,
-                const MergeWs& ws, hipStream_t s) {
+                const OrderWs& o, bool have_order, NbrList saved, hipStream_t s) {
   if (!gt) {
-    launch_atomic<DT, M, TH, KS>(q, P, table, g, gt, gq, nullptr, s);
+    launch_atomic<DT, M, TH, KS>(q, P, table, g, gt, gq, nullptr, nullptr, saved, s);
     return launched();
   }
-  const dim3 kgrid((unsigned)((P.L + THREADS - 1) / THREADS));
-  hipLaunchKernelGGL(k_cell_key<TH>, kgrid, dim3(THREADS), 0, s, q, P, ws.sort.k0, ws.sort.v0);
-  if (int rc = launched()) return rc;
-  uint32_t* keys;
-  uint2* perm;
-  if (int rc = radix_sort(ws.sort, P.N, s, &keys, &perm)) return rc;
-  hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(WAVE), 0, s, ws.shared, 0u);
-  const int64_t cb = (P.L + THREADS - 1) / THREADS;
-  hipLaunchKernelGGL(k_count_shared, dim3((unsigned)(cb < 512 ? cb : 512)), dim3(THREADS), 0, s,
-                     (const uint32_t*)keys, P.L, ws.shared);
-  launch_atomic<DT, M, TH, KS>(q, P, table, g, gt, gq, ws.shared, s);
+  if (!have_order)
+    if (int rc = build_order<TH>(q, P, o, s)) return rc;
+  launch_atomic<DT, M, TH, KS>(q, P, table, g, gt, gq, o.shared, nullptr, saved, s);
   if (int rc = launched()) return rc;
   // one batch of at most merge_t<KS>() lookups per workgroup
   Params Pm = P;
   Pm.lpw = P.lpw < merge_lpw<KS>() ? P.lpw : merge_lpw<KS>();
   const int64_t per_block = (int64_t)Pm.lpw * WAVES;
   const dim3 grid((unsigned)((P.L + per_block - 1) / per_block));
-  hipLaunchKernelGGL((k_backward_merged<DT, M, TH, KS>), grid, dim3(THREADS), 0, s, q, Pm, table, g, gt, gq,
-                     (const uint32_t*)keys, (const uint2*)perm, (const uint32_t*)ws.shared);
+  const uint32_t* keys = o.sort.ka;
+  const uint32_t* perm = o.sort.va;
+  if constexpr (!TH && KS == NB) {
+    if (saved.on()) {
+      hipLaunchKernelGGL((k_backward_merged<DT, M, false, NB, true>), grid, dim3(THREADS), 0, s, q, Pm, table, g, gt,
+                         gq, keys, perm, (const uint32_t*)o.shared, saved);
+      return launched();
+    }
+  }
+  hipLaunchKernelGGL((k_backward_merged<DT, M, TH, KS>), grid, dim3(THREADS), 0, s, q, Pm, table, g, gt, gq, keys,
+                     perm, (const uint32_t*)o.shared, saved);
   return launched();
 }
 
@@ -262,15 +379,15 @@ int merged_pass(const float* q, const Params& P, const void* table, const float*
 template <int DT, int M>
 struct BwdAtomicLaunch {
   static int go(const float* q, const Params& P, const void* table, const float* g, float* gt, float* gq, bool th,
-                int width, hipStream_t s) {
+                int width, const uint32_t* perm, NbrList saved, hipStream_t s) {
     if (th) {
-      launch_atomic<DT, M, true, NB>(q, P, table, g, gt, gq, nullptr, s);
+      launch_atomic<DT, M, true, NB>(q, P, table, g, gt, gq, nullptr, perm, saved, s);
     } else {
       switch (width) {
-        case 16: launch_atomic<DT, M, false, 16>(q, P, table, g, gt, gq, nullptr, s); break;
-        case 64: launch_atomic<DT, M, false, 64>(q, P, table, g, gt, gq, nullptr, s); break;
-        case KALL: launch_atomic<DT, M, false, KALL>(q, P, table, g, gt, gq, nullptr, s); break;
-        default: launch_atomic<DT, M, false, NB>(q, P, table, g, gt, gq, nullptr, s); break;
+        case 16: launch_atomic<DT, M, false, 16>(q, P, table, g, gt, gq, nullptr, perm, saved, s); break;
+        case 64: launch_atomic<DT, M, false, 64>(q, P, table, g, gt, gq, nullptr, perm, saved, s); break;
+        case KALL: launch_atomic<DT, M, false, KALL>(q, P, table, g, gt, gq, nullptr, perm, saved, s); break;
+        default: launch_atomic<DT, M, false, NB>(q, P, table, g, gt, gq, nullptr, perm, saved, s); break;
       }
     }
     return launched();
@@ -280,13 +397,13 @@ struct BwdAtomicLaunch {
 template <int DT, int M>
 struct BwdMergedLaunch {
   static int go(const float* q, const Params& P, const void* table, const float* g, float* gt, float* gq,
-                const MergeWs& ws, bool th, int width, hipStream_t s) {
-    if (th) return merged_pass<DT, M, true, NB>(q, P, table, g, gt, gq, ws, s);
+                const OrderWs& o, bool have_order, bool th, int width, NbrList saved, hipStream_t s) {
+    if (th) return merged_pass<DT, M, true, NB>(q, P, table, g, gt, gq, o, have_order, saved, s);
     switch (width) {
-      case 16: return merged_pass<DT, M, false, 16>(q, P, table, g, gt, gq, ws, s);
-      case 64: return merged_pass<DT, M, false, 64>(q, P, table, g, gt, gq, ws, s);
-      case KALL: return merged_pass<DT, M, false, KALL>(q, P, table, g, gt, gq, ws, s);
-      default: return merged_pass<DT, M, false, NB>(q, P, table, g, gt, gq, ws, s);
+      case 16: return merged_pass<DT, M, false, 16>(q, P, table, g, gt, gq, o, have_order, saved, s);
+      case 64: return merged_pass<DT, M, false, 64>(q, P, table, g, gt, gq, o, have_order, saved, s);
+      case KALL: return merged_pass<DT, M, false, KALL>(q, P, table, g, gt, gq, o, have_order, saved, s);
+      default: return merged_pass<DT, M, false, NB>(q, P, table, g, gt, gq, o, have_order, saved, s);
     }
   }
 };
@@ -294,26 +411,30 @@ struct BwdMergedLaunch {
 template <int DT, int M>
 struct BwdSortedLaunch {
   static int go(const float* q, const Params& P, const void* table, const float* g, float* gt, float* gq,
-                const SortWs& ws, bool th, hipStream_t s) {
+                const SortedWs& ws, bool th, NbrList saved, hipStream_t s) {
+    const dim3 grid(grid_for(P)), b(THREADS);
+    const uint32_t* const np = nullptr;
     if (th)
-      hipLaunchKernelGGL((k_backward<DT, M, true, true>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g,
-                         gt, gq, ws.k0, ws.v0, (const uint32_t*)nullptr);
+      hipLaunchKernelGGL((k_backward<DT, M, true, true>), grid, b, 0, s, q, P, table, g, gt, gq, ws.sort.ka,
+                         ws.sort.va, np, np, saved);
+    else if (saved.on())
+      hipLaunchKernelGGL((k_backward<DT, M, true, false, NB, false, true>), grid, b, 0, s, q, P, table, g, gt, gq,
+                         ws.sort.ka, ws.sort.va, np, np, saved);
     else
-      hipLaunchKernelGGL((k_backward<DT, M, true, false>), dim3(grid_for(P)), dim3(THREADS), 0, s, q, P, table, g,
-                         gt, gq, ws.k0, ws.v0, (const uint32_t*)nullptr);
+      hipLaunchKernelGGL((k_backward<DT, M, true, false>), grid, b, 0, s, q, P, table, g, gt, gq, ws.sort.ka,
+                         ws.sort.va, np, np, saved);
     int rc = launched();
     if (rc || !gt) return rc;
-    uint32_t* kin;
-    uint2* vin;
-    if ((rc = radix_sort(ws, P.N, s, &kin, &vin))) return rc;  // keys lie in [0, N]
-    // span: 256 pairs per group, fewer when that would leave CUs idle (about
-    // 32 groups per CU for 256 CUs)
-    int64_t span = (ws.n + 256 * 32 - 1) / (256 * 32);
-    span = span < SEG_BATCH ? SEG_BATCH : (span > SEG_SPAN ? SEG_SPAN : span);
-    const int64_t groups = (ws.n + span - 1) / span;
+    if ((rc = radix_sort<uint2, false>(ws.sort, P.N, s))) return rc;  // keys lie in [0, N]
+    const bool odd = radix_passes(P.N) & 1;
+    const uint32_t* keys = odd ? ws.sort.kb : ws.sort.ka;
+    const uint2* vals = odd ? ws.sort.vb : ws.sort.va;
     const int64_t per_block = THREADS / M;
-    hipLaunchKernelGGL((k_segreduce<M>), dim3((unsigned)((groups + per_block - 1) / per_block)), dim3(THREADS), 0, s,
-                       kin, vin, ws.n, P.N, g, gt, (int)span);
+    const unsigned blocks = (unsigned)((ws.groups + per_block - 1) / per_block);
+    hipLaunchKernelGGL((k_segreduce<M>), dim3(blocks), b, 0, s, keys, vals, ws.sort.n, P.N, g, gt, ws.span, ws.edge,
+                       ws.flags);
+    hipLaunchKernelGGL((k_segfix<M>), dim3(blocks), b, 0, s, keys, ws.sort.n, ws.span, (const float*)ws.edge,
+                       (const uint32_t*)ws.flags, ws.groups, gt);
     return launched();
   }
 };
@@ -331,31 +452,57 @@ struct FwdKLaunch {
       case 16: hipLaunchKernelGGL((k_forward_k<DT, M, 16>), g, b, 0, s, q, P, table, out); break;
       case 64: hipLaunchKernelGGL((k_forward_k<DT, M, 64>), g, b, 0, s, q, P, table, out); break;
       case KALL: hipLaunchKernelGGL((k_forward_k<DT, M, KALL>), g, b, 0, s, q, P, table, out); break;
-      default: hipLaunchKernelGGL((k_forward<DT, M, false>), g, b, 0, s, q, P, table, out); break;
+      default:
+        hipLaunchKernelGGL((k_forward<DT, M, false>), g, b, 0, s, q, P, table, out, (const uint32_t*)nullptr,
+                           NbrList{nullptr, nullptr, nullptr});
+        break;
     }
     return launched();
   }
 };
 
+// An order passed by the caller: 256-byte aligned and large enough for L
+// lookups; its positions (perm) then address the lookups.
+int check_order(const void* order, size_t bytes, int64_t L, OrderWs* o) {
+  if (!order) return LRAM_OK;
+  if ((reinterpret_cast<uintptr_t>(order) & 255) || bytes < order_layout(L, nullptr, nullptr)) return LRAM_EINVAL;
+  order_layout(L, o, reinterpret_cast<char*>(const_cast<void*>(order)));
+  return LRAM_OK;
+}
+
+// Saved lists: all three arrays or none, 4-byte aligned.
+int check_saved(const void* slot, const void* w, const void* code, NbrList* nl) {
+  const int given = (slot != nullptr) + (w != nullptr) + (code != nullptr);
+  if (given != 0 && given != 3) return LRAM_EINVAL;
+  if (misaligned4(slot) || misaligned4(w) || misaligned4(code)) return LRAM_EINVAL;
+  *nl = NbrList{(int32_t*)slot, (float*)w, (uint32_t*)code};
+  return LRAM_OK;
+}
+
 int forward_impl(const float* in, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype, int64_t N,
-                 int32_t m, void* out, bool th, hipStream_t stream) {
+                 int32_t m, void* out, const void* order, size_t order_bytes, NbrList save, bool th,
+                 hipStream_t stream) {
   int64_t L;
   Params P;
   int rc = check_common(in, B, H, K, &L, &P);
   if (rc) return rc;
   rc = check_table(table, dtype, N, m, P, L);
   if (rc) return rc;
+  OrderWs o{};
+  if ((rc = check_order(order, order_bytes, L, &o))) return rc;
   if (L == 0) return LRAM_OK;
   if (!out || misaligned16(out)) return LRAM_EINVAL;
-  return dispatch<FwdLaunch>(dtype, m, in, P, table, out, th, stream);
+  return dispatch<FwdLaunch>(dtype, m, in, P, table, out, th, order ? (const uint32_t*)o.sort.va : nullptr, save,
+                             stream);
 }
 
 int resolve_mode(int64_t B, int64_t H, int mode, int* resolved);
 
 // width: list width (NB for lram_backward and the activation layer).
 int backward_impl(const float* in, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
-                  int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_in, int mode,
-                  void* workspace, size_t ws_bytes, int width, bool th, hipStream_t stream) {
+                  int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_in, const void* order,
+                  size_t order_bytes, NbrList saved, int mode, void* workspace, size_t ws_bytes, int width, bool th,
+                  hipStream_t stream) {
   int64_t L;
   Params P;
   int rc = check_common(in, B, H, K, &L, &P);
@@ -364,26 +511,31 @@ int backward_impl(const float* in, int64_t B, int64_t H, const int32_t K[8], con
   if (rc) return rc;
   if ((rc = resolve_mode(B, H, mode, &mode))) return rc;
   if (mode == LRAM_SCATTER_SORTED && width != NB) return LRAM_EMODE;  // the sorted scatter takes k = 32
+  OrderWs o{};
+  if ((rc = check_order(order, order_bytes, L, &o))) return rc;
   if (L == 0) return LRAM_OK;
   if (!grad_out || misaligned16(grad_out)) return LRAM_EINVAL;
   if (!grad_table && !grad_in) return LRAM_EINVAL;
   if (grad_table && misaligned16(grad_table)) return LRAM_EINVAL;
   if (grad_in && misaligned16(grad_in)) return LRAM_EINVAL;
   if (mode == LRAM_SCATTER_ATOMIC)
-    return dispatch<BwdAtomicLaunch>(dtype, m, in, P, table, grad_out, grad_table, grad_in, th, width, stream);
+    return dispatch<BwdAtomicLaunch>(dtype, m, in, P, table, grad_out, grad_table, grad_in, th, width,
+                                     order ? (const uint32_t*)o.sort.va : nullptr, saved, stream);
   if (mode == LRAM_SCATTER_MERGED) {
-    const size_t need = merge_ws_layout(L, nullptr, nullptr);
-    if (!workspace || ws_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LRAM_EWORKSPACE;
-    MergeWs ws;
-    merge_ws_layout(L, &ws, reinterpret_cast<char*>(workspace));
-    return dispatch<BwdMergedLaunch>(dtype, m, in, P, table, grad_out, grad_table, grad_in, ws, th, width, stream);
+    if (!order) {
+      const size_t need = order_layout(L, nullptr, nullptr);
+      if (!workspace || ws_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LRAM_EWORKSPACE;
+      order_layout(L, &o, reinterpret_cast<char*>(workspace));
+    }
+    return dispatch<BwdMergedLaunch>(dtype, m, in, P, table, grad_out, grad_table, grad_in, o, order != nullptr, th,
+                                     width, saved, stream);
   }
   if (L * NB >= (int64_t(1) << 32)) return LRAM_EINVAL;  // the sorted scatter's pair positions are 32-bit
-  const size_t need = sort_ws_layout(L, nullptr, nullptr);
+  const size_t need = sorted_layout(L, m, nullptr, nullptr);
   if (!workspace || ws_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255)) return LRAM_EWORKSPACE;
-  SortWs ws;
-  sort_ws_layout(L, &ws, reinterpret_cast<char*>(workspace));
-  return dispatch<BwdSortedLaunch>(dtype, m, in, P, table, grad_out, grad_table, grad_in, ws, th, stream);
+  SortedWs ws;
+  sorted_layout(L, m, &ws, reinterpret_cast<char*>(workspace));
+  return dispatch<BwdSortedLaunch>(dtype, m, in, P, table, grad_out, grad_table, grad_in, ws, th, saved, stream);
 }
 
 int resolve_mode(int64_t B, int64_t H, int mode, int* resolved) {
@@ -393,16 +545,18 @@ int resolve_mode(int64_t B, int64_t H, int mode, int* resolved) {
   return LRAM_OK;
 }
 
+constexpr NbrList NO_LIST{nullptr, nullptr, nullptr};
+
 }  // namespace
 
 extern "C" {
 
-int lram_version(void) { return 100; }
+int lram_version(void) { return 200; }
 
 const char* lram_strerror(int status) {
   switch (status) {
     case LRAM_OK: return "ok";
-    case LRAM_EINVAL: return "invalid argument (null/misaligned pointer or negative size)";
+    case LRAM_EINVAL: return "invalid argument (null/misaligned pointer, negative size or undersized buffer)";
     case LRAM_EBADK: return "invalid torus: every K_i must be even, 2 <= K_i <= 8192, N = prod K_i < 2^31";
     case LRAM_EDTYPE: return "unsupported table dtype or value dimension m";
     case LRAM_EWORKSPACE: return "workspace missing or too small";
@@ -426,14 +580,39 @@ int lram_neighbors(const float* q, int64_t B, int64_t H, const int32_t K[8], int
   return launched();
 }
 
+int lram_order_bytes(int64_t B, int64_t H, size_t* bytes, size_t* keys_offset, size_t* perm_offset) {
+  if (!bytes || B < 0 || H < 0 || (H != 0 && B > INT64_MAX / H) || B * H > LMAX) return LRAM_EINVAL;
+  const int64_t L = B * H;
+  *bytes = order_layout(L, nullptr, nullptr);
+  if (keys_offset) *keys_offset = ORDER_KEYS_OFFSET;
+  if (perm_offset) *perm_offset = ORDER_KEYS_OFFSET + align256((size_t)L * 4);
+  return LRAM_OK;
+}
+
+int lram_order(const float* q, int64_t B, int64_t H, const int32_t K[8], void* order, size_t order_bytes,
+               void* stream) {
+  int64_t L;
+  Params P;
+  int rc = check_common(q, B, H, K, &L, &P);
+  if (rc) return rc;
+  if (!order) return LRAM_EINVAL;
+  OrderWs o;
+  if ((rc = check_order(order, order_bytes, L, &o))) return rc;
+  if (L == 0) return LRAM_OK;
+  return build_order<false>(q, P, o, (hipStream_t)stream);
+}
+
 int lram_forward(const float* q, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
-                 int64_t N, int32_t m, void* out, void* stream) {
-  return forward_impl(q, B, H, K, table, dtype, N, m, out, false, (hipStream_t)stream);
+                 int64_t N, int32_t m, void* out, const void* order, size_t order_bytes, int32_t* nbr_slot,
+                 float* nbr_w, uint32_t* nbr_code, void* stream) {
+  NbrList nl;
+  if (int rc = check_saved(nbr_slot, nbr_w, nbr_code, &nl)) return rc;
+  return forward_impl(q, B, H, K, table, dtype, N, m, out, order, order_bytes, nl, false, (hipStream_t)stream);
 }
 
 int lram_theta_forward(const float* z, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
                        int64_t N, int32_t m, void* out, void* stream) {
-  return forward_impl(z, B, H, K, table, dtype, N, m, out, true, (hipStream_t)stream);
+  return forward_impl(z, B, H, K, table, dtype, N, m, out, nullptr, 0, NO_LIST, true, (hipStream_t)stream);
 }
 
 int lram_theta_coords(const float* z, int64_t B, int64_t H, const int32_t K[8], float* q, float* s, void* stream) {
@@ -460,29 +639,28 @@ int lram_backward_workspace_bytes(int64_t B, int64_t H, int32_t m, int mode, siz
     *bytes = 0;
     return LRAM_OK;
   }
-  if (mode == LRAM_SCATTER_SORTED || mode == LRAM_SCATTER_MERGED) {
-    if (H != 0 && B > INT64_MAX / H / NB) return LRAM_EINVAL;
-    *bytes = mode == LRAM_SCATTER_SORTED ? sort_ws_layout(B * H, nullptr, nullptr)
-                                         : merge_ws_layout(B * H, nullptr, nullptr);
-    return LRAM_OK;
-  }
-  return LRAM_EMODE;
+  if (H != 0 && B > INT64_MAX / H / NB) return LRAM_EINVAL;
+  *bytes = mode == LRAM_SCATTER_SORTED ? sorted_layout(B * H, m, nullptr, nullptr)
+                                       : order_layout(B * H, nullptr, nullptr);
+  return LRAM_OK;
 }
 
 int lram_backward(const float* q, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
-                  int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_q, int mode,
+                  int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_q, const void* order,
+                  size_t order_bytes, const int32_t* nbr_slot, const float* nbr_w, const uint32_t* nbr_code, int mode,
                   void* workspace, size_t ws_bytes, void* stream) {
-  return backward_impl(q, B, H, K, table, dtype, N, m, grad_out, grad_table, grad_q, mode, workspace, ws_bytes,
-                       NB, false, (hipStream_t)stream);
+  NbrList nl;
+  if (int rc = check_saved(nbr_slot, nbr_w, nbr_code, &nl)) return rc;
+  return backward_impl(q, B, H, K, table, dtype, N, m, grad_out, grad_table, grad_q, order, order_bytes, nl, mode,
+                       workspace, ws_bytes, NB, false, (hipStream_t)stream);
 }
 
 int lram_theta_backward(const float* z, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
                         int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_z, int mode,
                         void* workspace, size_t ws_bytes, void* stream) {
-  return backward_impl(z, B, H, K, table, dtype, N, m, grad_out, grad_table, grad_z, mode, workspace, ws_bytes,
-                       NB, true, (hipStream_t)stream);
+  return backward_impl(z, B, H, K, table, dtype, N, m, grad_out, grad_table, grad_z, nullptr, 0, NO_LIST, mode,
+                       workspace, ws_bytes, NB, true, (hipStream_t)stream);
 }
-
 int lram_access_histogram(const float* q, int64_t B, int64_t H, const int32_t K[8], float* hist, void* stream) {
   int64_t L;
   Params P;
@@ -577,7 +755,8 @@ int lram_backward_k(const float* q, int64_t B, int64_t H, const int32_t K[8], co
                     int mode, void* workspace, size_t ws_bytes, void* stream) {
   const int width = list_width(k);
   if (!width) return LRAM_EINVAL;
-  return backward_impl(q, B, H, K, table, dtype, N, m, grad_out, grad_table, grad_q, mode, workspace, ws_bytes,
+  return backward_impl(q, B, H, K, table, dtype, N, m, grad_out, grad_table, grad_q, nullptr, 0, NO_LIST, mode,
+                       workspace, ws_bytes,
                        width, false, (hipStream_t)stream);
 }
 

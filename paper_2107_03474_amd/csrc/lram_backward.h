@@ -156,31 +156,43 @@ __device__ __forceinline__ void grad_query(const Frame& F, const WaveLds<KS>& W,
 // sorts last).
 // gate (nullable): the merged scatter's device-side choice -- this kernel does
 // nothing when the batch is merged instead (see merge_chosen).
-template <int DT, int M, bool EMIT, bool TH, int KS = NB>
+// ORD: visit the lookups in the order perm (as k_forward).
+// SAVED: the forward's lists (NbrList saved) replace the search.
+template <int DT, int M, bool EMIT, bool TH, int KS = NB, bool ORD = false, bool SAVED = false>
 __global__ void __launch_bounds__(THREADS) k_backward(const float* __restrict__ q, Params P,
                                                       const void* __restrict__ table,
                                                       const float* __restrict__ gout, float* __restrict__ gtab,
                                                       float* __restrict__ gq, uint32_t* __restrict__ pair_key,
-                                                      uint2* __restrict__ pair_val, const uint32_t* __restrict__ gate) {
+                                                      uint2* __restrict__ pair_val, const uint32_t* __restrict__ gate,
+                                                      const uint32_t* __restrict__ perm, NbrList saved) {
   static_assert(!EMIT || KS == NB, "the sorted scatter takes lists of 32");
+  static_assert(!(SAVED || ORD) || (KS == NB && !TH), "orders and saved lists serve the k = 32 lookup");
   __shared__ SearchLds<WAVE, KS> S;
   if (gate && merge_chosen(*gate, P.L)) return;
   WaveCtx c;
-  if (!wave_ctx(P, c)) return;
+  if (!wave_ctx(P, c, ORD)) return;
   const int lane = c.lane;
   Search<KS> srch(P, S.tab, S.wave[c.wave], c.wave, lane);
   WaveLds<KS>& W = S.wave[c.wave];
   Frame* FR = S.frames[c.wave];
-  phase_a<TH>(q, c.base, c.nl, P, FR, lane);
+  uint32_t my_l = 0;
+  if constexpr (ORD)
+    my_l = phase_a_perm<TH>(q, perm, c.base, c.nl, P, FR, lane);
+  else
+    phase_a<TH>(q, c.base, c.nl, P, FR, lane);
   const char* tb = reinterpret_cast<const char*>(table);
   for (int t = 0; t < c.nl; ++t) {
     const Frame& F = FR[t];
     const Sel sel = read_sel(F);
-    const int count = srch.run(F, sel, 0);
-    const int64_t l = c.base + t;
+    const int64_t l = ORD ? (int64_t)(uint32_t)__builtin_amdgcn_readlane(my_l, t) : c.base + t;
+    int count;
+    if constexpr (SAVED)
+      count = srch.load(F, sel, 0, saved, l, P.N);
+    else
+      count = srch.run(F, sel, 0);
     if (!EMIT && gtab && count > 0) scatter_atomic<M, KS>(W, count, gout, l, gtab, lane);
-    if (gq) grad_query<DT, M, TH, KS>(F, W, S.tab, count, tb, gout, l, lane, gq, q, P);
-    if (EMIT && gtab && lane < NB) {
+    if (gq && (!ORD || l < P.L)) grad_query<DT, M, TH, KS>(F, W, S.tab, count, tb, gout, l, lane, gq, q, P);
+    if (EMIT && gtab && lane < NB && (!ORD || l < P.L)) {
       const int32_t s = W.nbr[0][lane].slot;
       pair_key[l * NB + lane] = s >= 0 ? (uint32_t)s : P.N;
       pair_val[l * NB + lane] = make_uint2((uint32_t)l, __float_as_uint(W.wgt[0][lane]));

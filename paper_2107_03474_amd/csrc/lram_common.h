@@ -81,6 +81,35 @@ struct alignas(16) WaveLds {
   uint32_t hist[64];  // distance histogram of the selection, 64 buckets on [4, 8)
 };
 
+// Neighbour lists saved by the forward for the backward (any pointer null: no
+// list).  Entry j of lookup l sits at [l][j] in the search's own order, padding
+// included: slot (-1 for padding), weight, and code -- the point's coordinates
+// p in the fundamental-region frame of its query (Sec. 2.6: k = c + sigma pi^-1 p),
+// eight 3-bit fields p_r - CMIN, F position r in bits [3r, 3r + 3).
+struct NbrList {
+  int32_t* slot;
+  float* w;
+  uint32_t* code;
+  __host__ __device__ bool on() const { return slot != nullptr; }
+};
+
+// Packed candidate bytes (4 (p_r - CMIN) + 64 w per F position) <-> code.
+__device__ __forceinline__ uint32_t code_of(uint32_t lo, uint32_t hi) {
+  auto squeeze = [](uint32_t v) {
+    v = (v >> 2) & 0x07070707u;
+    return (v & 0x7u) | ((v >> 5) & 0x38u) | ((v >> 10) & 0x1C0u) | ((v >> 15) & 0xE00u);
+  };
+  return squeeze(lo) | (squeeze(hi) << 12);
+}
+__device__ __forceinline__ void bytes_of(uint32_t code, uint32_t wbyte, uint32_t& lo, uint32_t& hi) {
+  auto spread = [](uint32_t c) {
+    return (c & 0x7u) | ((c & 0x38u) << 5) | ((c & 0x1C0u) << 10) | ((c & 0xE00u) << 15);
+  };
+  const uint32_t wb = wbyte * 0x01010101u;
+  lo = (spread(code & 0xFFFu) << 2) + wb;
+  hi = (spread((code >> 12) & 0xFFFu) << 2) + wb;
+}
+
 // per-query tables, [coordinate i][wave w][value v] -> byte i*256 + w*64 + 4v
 struct alignas(16) Tables {
   float qt[8 * 64];

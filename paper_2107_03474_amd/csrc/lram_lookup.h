@@ -16,10 +16,13 @@ struct WaveCtx {
   int nl;
 };
 
-__device__ __forceinline__ bool wave_ctx(const Params P, WaveCtx& c) {
+// xcd: take the workgroups' ranges XCD-contiguously (for lookups visited in a
+// locality order, so that neighbouring ranges share an L2).
+__device__ __forceinline__ bool wave_ctx(const Params P, WaveCtx& c, bool xcd = false) {
   c.wave = threadIdx.x / WAVE;
   c.lane = threadIdx.x % WAVE;
-  c.base = ((int64_t)blockIdx.x * WAVES + c.wave) * P.lpw;
+  const int64_t blk = xcd ? xcd_block() : (int64_t)blockIdx.x;
+  c.base = (blk * WAVES + c.wave) * P.lpw;
   if (c.base >= P.L) return false;
   c.nl = (int)min<int64_t>(P.lpw, P.L - c.base);
   return true;
@@ -191,26 +194,39 @@ __device__ __forceinline__ void fwd_consume(const WaveLds<NB, 2>& W, int buf, in
 
 // TH: the input is the activation layer's z [L][16] instead of q [L][8]; the
 // scale s is folded into the weights by the search.
-template <int DT, int M, bool TH>
+// ORD: visit the lookups in the order perm (position -> lookup, e.g. sorted
+// by closest lattice point, so that lookups sharing rows run close together
+// in time and on the same XCD); outputs still go to the lookup's row.
+// SAVE: write every lookup's list for the backward (NbrList).
+template <int DT, int M, bool TH, bool ORD = false, bool SAVE = false>
 __global__ void __launch_bounds__(THREADS) k_forward(const float* __restrict__ q, Params P,
-                                                     const void* __restrict__ table, void* __restrict__ out) {
+                                                     const void* __restrict__ table, void* __restrict__ out,
+                                                     const uint32_t* __restrict__ perm, NbrList save) {
   using G = FwdGeom<DT, M>;
   __shared__ SearchLds<WAVE, NB, 2> S;
   WaveCtx c;
-  if (!wave_ctx(P, c)) return;
+  if (!wave_ctx(P, c, ORD)) return;
   Search<NB, 2> srch(P, S.tab, S.wave[c.wave], c.wave, c.lane);
   WaveLds<NB, 2>& W = S.wave[c.wave];
   Frame* FR = S.frames[c.wave];
-  phase_a<TH>(q, c.base, c.nl, P, FR, c.lane);
+  uint32_t my_l = 0;
+  if constexpr (ORD)
+    my_l = phase_a_perm<TH>(q, perm, c.base, c.nl, P, FR, c.lane);
+  else
+    phase_a<TH>(q, c.base, c.nl, P, FR, c.lane);
   const char* tb = reinterpret_cast<const char*>(table);
   uint32_t v[G::NI][G::DW];
   srch.run(FR[0], read_sel(FR[0]), 0);
   fwd_issue<DT, M, NB>(tb, W, 0, c.lane, v);
   for (int t = 0; t < c.nl; ++t) {
     const int buf = t & 1;
+    const int64_t l = ORD ? (int64_t)(uint32_t)__builtin_amdgcn_readlane(my_l, t) : c.base + t;
     // search lookup t+1 while the rows of lookup t are in flight
     if (t + 1 < c.nl) srch.run(FR[t + 1], read_sel(FR[t + 1]), buf ^ 1);
-    fwd_consume<DT, M>(W, buf, c.lane, c.base + t, v, out);
+    if (!ORD || l < P.L) {
+      fwd_consume<DT, M>(W, buf, c.lane, l, v, out);
+      if constexpr (SAVE) srch.save(buf, save, l);
+    }
     if (t + 1 < c.nl) fwd_issue<DT, M, NB>(tb, W, buf ^ 1, c.lane, v);
   }
 }

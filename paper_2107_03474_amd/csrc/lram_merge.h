@@ -16,10 +16,10 @@ namespace {
 // location of the batch.
 
 // key[l] = location of the closest point of Lambda to q_l (N for a non-finite
-// query), val[l] = (l, 0).
+// query).
 template <bool TH>
 __global__ void __launch_bounds__(THREADS) k_cell_key(const float* __restrict__ q, Params P,
-                                                      uint32_t* __restrict__ key, uint2* __restrict__ val) {
+                                                      uint32_t* __restrict__ key) {
   const int64_t l = (int64_t)blockIdx.x * THREADS + threadIdx.x;
   if (l >= P.L) return;
   float x[8], qq[8], scale;
@@ -32,14 +32,17 @@ __global__ void __launch_bounds__(THREADS) k_cell_key(const float* __restrict__ 
     uint32_t acc = eps ? P.N : 0u;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-      int y = (c[i] - eps) >> 1;  // in [-1, K_i]
-      y = y < 0 ? y + P.K[i] : (y >= P.K[i] ? y - P.K[i] : y);
+      // |x_i| < 2 K_i and |x_i - c_i| <= 1 put y within [-K_i - 1, K_i]: two
+      // periods up or one down bring it into [0, K_i) (K_i = 2 included)
+      int y = (c[i] - eps) >> 1;
+      y += y < 0 ? P.K[i] : 0;
+      y += y < 0 ? P.K[i] : 0;
+      y -= y >= P.K[i] ? P.K[i] : 0;
       acc += (uint32_t)y * P.S[i];
     }
     loc = acc >> 1;
   }
   key[l] = loc;
-  val[l] = make_uint2((uint32_t)l, 0u);
 }
 
 // Activation layer coordinates: q[l] (8 fp32) and scale s[l] as the lookups see them.
@@ -162,14 +165,15 @@ constexpr int merge_waves_per_simd() {
 // A batch in which fewer than a tenth of the lookups share their closest
 // point with a neighbour in the order (queries spread thinly over the torus)
 // has little to merge: it scatters with per-lookup atomics instead.
-template <int DT, int M, bool TH, int KS = NB>
+// SAVED: the forward's lists (NbrList saved) replace the search.
+template <int DT, int M, bool TH, int KS = NB, bool SAVED = false>
 __global__ void __launch_bounds__(THREADS, (merge_waves_per_simd<DT, M, KS>())) k_backward_merged(const float* __restrict__ q, Params P,
                                                              const void* __restrict__ table,
                                                              const float* __restrict__ gout,
                                                              float* __restrict__ gtab, float* __restrict__ gq,
                                                              const uint32_t* __restrict__ skey,
-                                                             const uint2* __restrict__ perm,
-                                                             const uint32_t* __restrict__ gate) {
+                                                             const uint32_t* __restrict__ perm,
+                                                             const uint32_t* __restrict__ gate, NbrList saved) {
   __shared__ FusedLds<M, KS> S;
   if (!merge_chosen(*gate, P.L)) return;  // the batch is scattered by k_backward instead
   const int t = threadIdx.x, wave = t / WAVE, lane = t % WAVE;
@@ -195,10 +199,14 @@ __global__ void __launch_bounds__(THREADS, (merge_waves_per_simd<DT, M, KS>())) 
       for (int i = 0; i < nl; ++i) {
         const Frame& F = FR[i];
         const Sel sel = read_sel(F);
-        const int count = srch.run(F, sel, 0);
-        const int64_t l = (int64_t)__builtin_amdgcn_readlane(my_l, i);
+        const int64_t l = (int64_t)(uint32_t)__builtin_amdgcn_readlane(my_l, i);
+        int count;
+        if constexpr (SAVED)
+          count = srch.load(F, sel, 0, saved, l, P.N);
+        else
+          count = srch.run(F, sel, 0);
         if (!merge && count > 0) scatter_atomic<M, KS>(W, count, gout, l, gtab, lane);
-        if (gq) grad_query<DT, M, TH, KS>(F, W, S.b.search.tab, count, tb, gout, l, lane, gq, q, P);
+        if (gq && l < P.L) grad_query<DT, M, TH, KS>(F, W, S.b.search.tab, count, tb, gout, l, lane, gq, q, P);
         if (merge && !COMPACT) {
 #pragma unroll
           for (int j = lane; j < KS; j += WAVE) {
@@ -254,8 +262,9 @@ __global__ void __launch_bounds__(THREADS, (merge_waves_per_simd<DT, M, KS>())) 
   for (int k = 0; k < MERGE_HPT / 2; ++k) MW.cnt[k * THREADS + t] = 0u;
   for (int i = t; i < nt * (M / 4); i += THREADS) {
     const int r = i / (M / 4), c4 = i % (M / 4);
-    const uint32_t l = perm[bbase + r].x;
-    reinterpret_cast<float4*>(MW.g[r])[c4] = reinterpret_cast<const float4*>(gout + (size_t)l * M)[c4];
+    const uint32_t l = perm[bbase + r];
+    reinterpret_cast<float4*>(MW.g[r])[c4] =
+        l < P.L ? reinterpret_cast<const float4*>(gout + (size_t)l * M)[c4] : make_float4(0.f, 0.f, 0.f, 0.f);
   }
   __syncthreads();
   // insert every pair's location; keep (entry, rank among the entry's pairs)

@@ -561,6 +561,55 @@ struct Search {
     wave_lds_sync();
     return count;
   }
+
+  // The list of lookup l saved by the forward (NbrList), in place of run():
+  // the per-query tables are rebuilt from the frame (the coordinate errors for
+  // dq) and each entry's recipe distance is recomputed from its code exactly
+  // as run() formed it.  Entries whose slot lies outside [0, N) count as
+  // padding, so no list content can address outside the value table.
+  __device__ int load(const Frame& F, const Sel& sel, int buf, const NbrList nl, int64_t l, uint32_t N) {
+    static_assert(KS == NB, "saved lists hold the closest 32");
+    const bool valid = (sel.misc & 0x100u) != 0;
+    if (valid) {
+      build_tables(F, sel.misc);
+      wave_lds_sync();
+    }
+    bool real = false;
+    if (lane < KS) {
+      const size_t o = (size_t)l * KS + lane;
+      const int32_t s = valid ? nl.slot[o] : -1;
+      real = s >= 0 && (uint32_t)s < N;
+      Nbr& n = W.nbr[buf][lane];
+      if (real) {
+        uint32_t l8, h8;
+        bytes_of(nl.code[o] & 0xFFFFFFu, wbyte, l8, h8);
+        n.lo = l8;
+        n.hi = h8;
+        n.dbits = __float_as_uint(cand_d2(S.qt, l8, h8, sel));
+        n.slot = s;
+        W.wgt[buf][lane] = nl.w[o];
+      } else {
+        n.lo = n.hi = 0;
+        n.dbits = KEY_INF;
+        n.slot = -1;
+        W.wgt[buf][lane] = 0.0f;
+      }
+    }
+    wave_lds_sync();
+    return __popcll(__ballot(real));
+  }
+
+  // Writes list `buf` of lookup l to the saved lists (lanes 0..KS-1).
+  __device__ __forceinline__ void save(int buf, const NbrList nl, int64_t l) const {
+    static_assert(KS == NB, "saved lists hold the closest 32");
+    if (lane < KS) {
+      const size_t o = (size_t)l * KS + lane;
+      const Nbr n = W.nbr[buf][lane];
+      nl.slot[o] = n.slot;
+      nl.w[o] = W.wgt[buf][lane];
+      nl.code[o] = n.slot >= 0 ? code_of(n.lo, n.hi) : 0u;
+    }
+  }
 };
 
 // Input floats per lookup: q (8) or z (16, the activation layer).
@@ -576,14 +625,17 @@ __device__ __forceinline__ void phase_a(const float* __restrict__ in, int64_t ba
 }
 
 // Same, for the lookups perm[base .. base + nl) of a reordered batch; returns
-// this lane's lookup index (lane t holds the lookup of position base + t).
+// this lane's lookup index (lane t holds the lookup of position base + t).  An
+// index outside [0, L) (an order not written for these lookups) gets an empty
+// list, and the kernels write nothing for it.
 template <bool TH>
-__device__ __forceinline__ uint32_t phase_a_perm(const float* __restrict__ in, const uint2* __restrict__ perm,
+__device__ __forceinline__ uint32_t phase_a_perm(const float* __restrict__ in, const uint32_t* __restrict__ perm,
                                                  int64_t base, int nl, const Params P, Frame* frames, int lane) {
   uint32_t l = 0;
   if (lane < nl) {
-    l = perm[base + lane].x;
-    make_frame<TH>(in + (size_t)l * in_stride<TH>(), true, P, frames[lane]);
+    l = perm[base + lane];
+    const bool ok = (int64_t)l < P.L;
+    make_frame<TH>(in + (size_t)(ok ? l : 0u) * in_stride<TH>(), ok, P, frames[lane]);
   }
   wave_lds_sync();
   return l;

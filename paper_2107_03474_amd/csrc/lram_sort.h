@@ -104,11 +104,15 @@ __global__ void __launch_bounds__(THREADS) k_scan_add(uint32_t* __restrict__ a, 
 // match inside the wave plus per-(wave, digit) counts carried across rounds.
 // The tile is first ordered by digit in LDS (a 2-byte permutation), then
 // written out in that order so that consecutive threads store consecutive
-// addresses of a digit's output run.
+// addresses of a digit's output run.  V is the payload: the lookup index
+// (uint32_t; IDENT: the first pass's payload is the element's own index, so it
+// is never stored) or a (lookup, weight) pair (uint2).
+template <typename V, bool IDENT>
 __global__ void __launch_bounds__(THREADS) k_radix_scatter(const uint32_t* __restrict__ kin,
-                                                           const uint2* __restrict__ vin, int64_t n, int shift,
+                                                           const V* __restrict__ vin, int64_t n, int shift,
                                                            const uint32_t* __restrict__ offs, int nblocks,
-                                                           uint32_t* __restrict__ kout, uint2* __restrict__ vout) {
+                                                           uint32_t* __restrict__ kout, V* __restrict__ vout) {
+  static_assert(!IDENT || sizeof(V) == 4, "identity payloads are lookup indices");
   __shared__ uint32_t run_cnt[RADIX];
   __shared__ uint32_t wave_cnt[WAVES][RADIX];
   __shared__ uint32_t tile_start[RADIX];
@@ -183,47 +187,53 @@ __global__ void __launch_bounds__(THREADS) k_radix_scatter(const uint32_t* __res
       const uint32_t d = (key >> shift) & (RADIX - 1);
       const uint32_t pos = glob_off[d] + (uint32_t)j - tile_start[d];
       kout[pos] = key;
-      vout[pos] = vin[base + src];
+      if constexpr (IDENT)
+        vout[pos] = (V)(base + src);
+      else
+        vout[pos] = vin[base + src];
     }
   }
 }
 
-// Segmented reduction of the sorted pairs.  A group of M lanes (lane = column
-// of the gradient row) owns a span of consecutive pairs (256, fewer for small
-// batches so that every CU gets work) and walks it in
+// Segmented reduction of the sorted pairs, bit-reproducible.  A group of M
+// lanes (lane = column of the gradient row) owns a span of consecutive pairs
+// (256, fewer for small batches so that every CU gets work) and walks it in
 // order, prefetching 16 pairs and their upstream-gradient rows at a time; it
-// accumulates w * G[lookup] while the location stays the same and writes each
-// finished run of one location with a single plain read-modify-write when the
-// run lies inside the span (no other group touches that row), or with fp32
-// atomics for the runs cut by the span edges (so a hot location costs one
-// atomic row per span of updates and never serialises one group).
+// accumulates w * G[lookup] while the location stays the same.  A run of one
+// location that lies inside the span is written with one plain
+// read-modify-write (no other group touches that row).  The partial sums of
+// runs cut by the span's edges go to the span's two edge rows instead (head:
+// the run that began in an earlier span, or the whole span when one run
+// passes through it; tail: the run that begins here and continues), and
+// k_segfix adds them in span order, one owner per cut run -- so every row's
+// sum is formed in the same order on every call.
 constexpr int SEG_SPAN = 256;
 constexpr int SEG_BATCH = 16;
-
-template <int M>
-__device__ __forceinline__ void seg_flush(float* __restrict__ gtab, uint32_t key, int col, float acc, bool plain) {
-  float* dst = gtab + (size_t)key * M + col;
-  if (plain)
-    *dst += acc;
-  else
-    unsafeAtomicAdd(dst, acc);
-}
+constexpr uint32_t SEG_HEAD = 1u;     // edge row 0 holds the partial of a run that began earlier
+constexpr uint32_t SEG_TAIL = 2u;     // edge row 1 holds the partial of a run that began here and continues
+constexpr uint32_t SEG_THROUGH = 4u;  // one run covers the whole span and continues past it (partial in row 0)
 
 template <int M>
 __global__ void __launch_bounds__(THREADS) k_segreduce(const uint32_t* __restrict__ keys,
                                                        const uint2* __restrict__ vals, int64_t n, uint32_t N,
                                                        const float* __restrict__ gout, float* __restrict__ gtab,
-                                                       int span) {
+                                                       int span, float* __restrict__ edge, uint32_t* __restrict__ flags) {
   const int64_t group = ((int64_t)blockIdx.x * THREADS + threadIdx.x) / M;
   const int col = threadIdx.x % M;
   const int64_t b = group * span;
   if (b >= n) return;
   const int64_t e = min<int64_t>(n, b + span);
   uint32_t cur = keys[b];
-  if (cur >= N) return;  // padding sorts last
-  bool head_here = (b == 0) || keys[b - 1] != cur;
+  uint32_t fl = 0;
+  if (cur >= N) {  // padding sorts last
+    if (col == 0) flags[group] = 0;
+    return;
+  }
+  const bool head_cut = b > 0 && keys[b - 1] == cur;
+  bool first = true;  // the current run is the span's first
   float acc = 0.0f;
-  bool pad = false;  // reached the padding (key N), which sorts last
+  bool pad = false;   // reached the padding (key N), which sorts last
+  float* erow = edge + (size_t)group * 2 * M + col;
   for (int64_t p = b; p < e && !pad; p += SEG_BATCH) {
     uint32_t k[SEG_BATCH];
     float wv[SEG_BATCH], g[SEG_BATCH];
@@ -242,23 +252,55 @@ __global__ void __launch_bounds__(THREADS) k_segreduce(const uint32_t* __restric
           pad = true;  // the current run ended just before the padding
         } else {
           if (k[u] != cur) {
-            seg_flush<M>(gtab, cur, col, acc, head_here);  // ended inside the span
+            // the run of cur ended inside the span
+            if (first && head_cut) {
+              erow[0] = acc;
+              fl |= SEG_HEAD;
+            } else {
+              gtab[(size_t)cur * M + col] += acc;
+            }
+            first = false;
             cur = k[u];
             acc = 0.0f;
-            head_here = true;
           }
           acc = fmaf(wv[u], g[u], acc);
         }
       }
     }
   }
-  if (pad) {
-    seg_flush<M>(gtab, cur, col, acc, head_here);
-    return;
+  // the span's last run: cut by the end unless the padding or the batch end
+  // follows it
+  const bool tail_cut = !pad && e < n && keys[e] == cur;
+  if (first && head_cut) {
+    erow[0] = acc;
+    fl |= tail_cut ? (SEG_HEAD | SEG_THROUGH) : SEG_HEAD;
+  } else if (tail_cut) {
+    erow[M] = acc;
+    fl |= SEG_TAIL;
+  } else {
+    gtab[(size_t)cur * M + col] += acc;
   }
-  // the span's last run: plain only if it also ends inside the span
-  const bool ends_here = (e == n) || keys[e] != cur;
-  seg_flush<M>(gtab, cur, col, acc, head_here && ends_here);
+  if (col == 0) flags[group] = fl;
+}
+
+// Runs cut by span edges: the span where a run begins (SEG_TAIL) adds, in span
+// order, its tail partial, the partials of the spans the run passes through
+// and the head partial of the span where it ends, and writes the row once
+// (plain read-modify-write: no other group touches it).
+template <int M>
+__global__ void __launch_bounds__(THREADS) k_segfix(const uint32_t* __restrict__ keys, int64_t n, int span,
+                                                    const float* __restrict__ edge, const uint32_t* __restrict__ flags,
+                                                    int64_t groups, float* __restrict__ gtab) {
+  const int64_t group = ((int64_t)blockIdx.x * THREADS + threadIdx.x) / M;
+  const int col = threadIdx.x % M;
+  if (group >= groups || !(flags[group] & SEG_TAIL)) return;
+  const uint32_t key = keys[min<int64_t>(n, (group + 1) * span) - 1];
+  float acc = edge[(size_t)group * 2 * M + M + col];
+  for (int64_t g = group + 1; g < groups; ++g) {
+    acc += edge[(size_t)g * 2 * M + col];
+    if (!(flags[g] & SEG_THROUGH)) break;
+  }
+  gtab[(size_t)key * M + col] += acc;
 }
 
 }  // namespace

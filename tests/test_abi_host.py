@@ -49,8 +49,9 @@ FAKE = ctypes.c_void_p(0x10000)      # never dereferenced: validation fails firs
 FAKE_MIS = ctypes.c_void_p(0x10004)  # misaligned
 
 
-def _fwd(lib, q=FAKE, B=4, H=1, K=K4, table=FAKE, dtype=0, N=4 ** 8, m=32, out=FAKE):
-    return lib.lram_forward(q, B, H, K, table, dtype, N, m, out, None)
+def _fwd(lib, q=FAKE, B=4, H=1, K=K4, table=FAKE, dtype=0, N=4 ** 8, m=32, out=FAKE, order=None, ob=0, slot=None,
+         w=None, code=None):
+    return lib.lram_forward(q, B, H, K, table, dtype, N, m, out, order, ob, slot, w, code, None)
 
 
 def test_forward_validation(lib):
@@ -74,6 +75,37 @@ def test_forward_validation(lib):
     assert _fwd(lib, q=None, table=None, out=None, H=0) == 0
 
 
+def test_order_and_saved_list_validation(lib):
+    """Order buffers are 256-byte aligned and large enough for the call's
+    lookups; saved lists come as all three arrays or none, 4-byte aligned."""
+    n, ko, po = ctypes.c_size_t(0), ctypes.c_size_t(0), ctypes.c_size_t(0)
+    assert lib.lram_order_bytes(1000, 3, ctypes.byref(n), ctypes.byref(ko), ctypes.byref(po)) == 0
+    assert ko.value == 256 and po.value == 256 + 12032 and n.value >= po.value + 12000
+    assert lib.lram_order_bytes(-1, 3, ctypes.byref(n), None, None) == 1
+    assert lib.lram_order_bytes(1 << 31, 1, ctypes.byref(n), None, None) == 1
+    need = ctypes.c_size_t(0)
+    assert lib.lram_order_bytes(4, 1, ctypes.byref(need), None, None) == 0
+    ORD = ctypes.c_void_p(0x20000)
+    assert lib.lram_order(FAKE, 4, 1, K4, None, need.value, None) == 1
+    assert lib.lram_order(FAKE, 4, 1, K4, ORD, need.value - 1, None) == 1                 # undersized
+    assert lib.lram_order(FAKE, 4, 1, K4, ctypes.c_void_p(0x20010), need.value, None) == 1  # misaligned
+    assert lib.lram_order(FAKE, 4, 1, (ctypes.c_int32 * 8)(*([3] * 8)), ORD, need.value, None) == 2
+    assert lib.lram_order(None, 0, 1, K4, ORD, need.value, None) == 0
+    assert _fwd(lib, order=ORD, ob=need.value - 256) == 1
+    assert _fwd(lib, order=ctypes.c_void_p(0x20080), ob=need.value) == 1
+    assert _fwd(lib, slot=FAKE, w=FAKE) == 1                                   # lists incomplete
+    assert _fwd(lib, slot=FAKE, w=FAKE, code=ctypes.c_void_p(0x10002)) == 1    # misaligned
+    assert _fwd(lib, slot=FAKE, code=FAKE) == 1
+
+    def bwd(order=None, ob=0, slot=None, w=None, code=None):
+        return lib.lram_backward(FAKE, 4, 1, K4, FAKE, 0, 4 ** 8, 32, FAKE, FAKE, FAKE, order, ob, slot, w, code, 2,
+                                 None, 0, None)
+
+    assert bwd(slot=FAKE) == 1
+    assert bwd(order=ORD, ob=need.value - 1) == 1
+    assert bwd() == 4                                  # merged without an order needs a workspace
+
+
 def test_neighbors_validation(lib):
     assert lib.lram_neighbors(FAKE, 4, 1, (ctypes.c_int32 * 8)(*([5] * 8)), FAKE, FAKE, None, None) == 2
     assert lib.lram_neighbors(FAKE, 4, 1, K4, None, FAKE, None, None) == 1
@@ -87,7 +119,8 @@ def test_neighbors_validation(lib):
 
 def test_backward_validation(lib):
     def bwd(grad_out=FAKE, gt=FAKE, gq=FAKE, mode=0, K=K4, B=4, ws=None, wsb=0):
-        return lib.lram_backward(FAKE, B, 1, K, FAKE, 0, 4 ** 8, 32, grad_out, gt, gq, mode, ws, wsb, None)
+        return lib.lram_backward(FAKE, B, 1, K, FAKE, 0, 4 ** 8, 32, grad_out, gt, gq, None, 0, None, None, None, mode,
+                                 ws, wsb, None)
 
     assert bwd(mode=9) == 5
     assert bwd(grad_out=None) == 1
@@ -178,7 +211,7 @@ def test_auto_mode(lib):
     assert lib.lram_scatter_mode_resolved(-1, 1, 0, ctypes.byref(r)) == 1
     n = ctypes.c_size_t(1)
     assert lib.lram_backward_workspace_bytes(4, 1, 32, 3, ctypes.byref(n)) == 0 and n.value == 0
-    assert lib.lram_backward_workspace_bytes(8192, 16, 32, 3, ctypes.byref(n)) == 0 and n.value >= 131072 * 24
+    assert lib.lram_backward_workspace_bytes(8192, 16, 32, 3, ctypes.byref(n)) == 0 and n.value >= 131072 * 16
 
 
 def test_no_oracle_in_product():

@@ -11,7 +11,8 @@ checks sampled outputs one by one:
     <= 1e-4 (fp32 atomics in any order vs fp64, up to ~3e4 terms per hot row);
   * sampled locations no lookup touches: exactly 0;
   * on the billion-location workload the atomic and sorted scatters are run
-    too and checked the same way (dq bit-identical across the three).
+    too and checked the same way (dq bit-identical across the three), the
+    sorted one twice: a million sampled rows bit-identical between the calls.
 """
 import gc
 
@@ -132,7 +133,12 @@ def test_full_size(name):
     if name == "k14-m32-bf16-zipf":
         # the other two scatters at the same scale, against the same oracle rows
         pick_t = torch.from_numpy(pick).to(DEV)
-        for mode in ("atomic", "sorted"):
+        # rows checked bit for bit across two sorted-scatter calls: the sampled
+        # rows and a million random touched ones
+        tidx = torch.nonzero(all_touched).reshape(-1)
+        rep = torch.cat([pick_t, tidx[torch.randint(0, tidx.numel(), (1 << 20,), device=DEV)]])
+        first = None
+        for mode in ("atomic", "sorted", "sorted"):
             gtab.zero_()
             gq2 = torch.empty_like(gq)
             lram.backward(q, table, w.K, G, grad_table=gtab, grad_q=gq2, mode=mode)
@@ -142,6 +148,12 @@ def test_full_size(name):
             _say("dV (%s scatter): max rel err %.2e over %d sampled rows" % (mode, err.max(), pick.size))
             assert err.max() <= 1e-4
             assert torch.count_nonzero(gtab[cold]).item() == 0
+            if mode == "sorted":
+                rows_now = gtab[rep].cpu()
+                if first is None:
+                    first = rows_now
+                else:
+                    assert torch.equal(rows_now, first)  # the sorted scatter is bit-reproducible
             del gq2
     del table, gtab, G, out, slot, wgt, d2, all_touched
     gc.collect()
