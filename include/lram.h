@@ -212,6 +212,25 @@ int lram_backward(const float* q, int64_t B, int64_t H, const int32_t K[8], cons
                   int mode, void* workspace, size_t ws_bytes, void* stream);
 
 /*
+ * lram_backward_noalloc -- lram_backward (no order, no saved lists) for callers
+ * that cannot allocate device memory: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation.  The workspace of the
+ * sorted and merged scatters is a static array inside the library, one per
+ * GPU, LRAM_STATIC_SCRATCH_BYTES long, held from the library's first use on a
+ * GPU until the process ends; the call itself allocates nothing.  Up to
+ * 5.1 M lookups fit the merged scatter's order (the billion-location
+ * workload's 4,194,304 included), about 100 K the sorted scatter's pairs;
+ * larger calls return LRAM_EWORKSPACE (the atomic mode needs no workspace and
+ * takes any size).  Every call on a GPU shares that GPU's array: calls that
+ * may overlap on one GPU (other streams, other host threads) race on it and
+ * must not be issued.  The stream must belong to the current device.
+ */
+#define LRAM_STATIC_SCRATCH_BYTES ((size_t)80 << 20)
+int lram_backward_noalloc(const float* q, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
+                          int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_q, int mode,
+                          void* stream);
+
+/*
  * Training-side companions.
  *
  * lram_access_histogram -- hist[s] += sum of the kernel weights w_j of the

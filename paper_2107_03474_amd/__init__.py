@@ -25,7 +25,7 @@ __all__ = ["neighbors", "forward", "backward", "backward_workspace_bytes", "look
            "SCATTER_MERGED", "SCATTER_AUTO", "resolved_mode", "NB",
            "theta_coords", "theta_forward", "theta_backward", "ThetaLookup", "theta", "ALL", "MAX_SUPPORT",
            "list_width", "access_histogram", "access_stats", "sparse_adam", "SparseAdam", "Lists", "new_lists",
-           "order", "order_layout", "order_view"]
+           "order", "order_layout", "order_view", "backward_noalloc"]
 
 NB = 32
 F32, BF16 = 0, 1
@@ -76,6 +76,8 @@ def load():
             lib.lram_backward.argtypes = [P, I64, I64, P, P, I, I64, I32, P, P, P, P, ctypes.c_size_t, P, P, P, I, P,
                                           ctypes.c_size_t, P]
             lib.lram_backward.restype = I
+            lib.lram_backward_noalloc.argtypes = [P, I64, I64, P, P, I, I64, I32, P, P, P, I, P]
+            lib.lram_backward_noalloc.restype = I
             lib.lram_neighbors_k.argtypes = [P, I64, I64, P, I32, P, P, P, P]
             lib.lram_neighbors_k.restype = I
             lib.lram_forward_k.argtypes = [P, I64, I64, P, P, I, I64, I32, I32, P, P]
@@ -321,6 +323,22 @@ def backward(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], grad_out: t
         _check(lib.lram_backward(*head, *grads, *_order(order, q), *_lists(lists, q), mode_i,
                                  *_workspace(workspace, q), _stream(q)))
     return (grad_table if grad_table is not False else None), gq
+
+
+def backward_noalloc(q: torch.Tensor, table: torch.Tensor, K: Sequence[int], grad_out: torch.Tensor,
+                     grad_table: torch.Tensor, grad_q: Optional[torch.Tensor] = None, mode="auto"):
+    """lram_backward_noalloc: ``backward`` whose scatter workspace is the library's
+    static per-GPU array (nothing allocated by the call).  grad_table [N, m] fp32
+    is accumulated into, grad_q [..., 8] fp32 (nullable) overwritten."""
+    lib = load()
+    B, H = _bh(q)
+    N, m = _table_shape(table)
+    _check(lib.lram_backward_noalloc(
+        _dev(q, "q", torch.float32), B, H, _K(K), _dev(table, "table", like=q), _table_dtype(table), N, m,
+        _dev(grad_out, "grad_out", torch.float32, q.shape[:-1] + (m,), like=q),
+        _dev(grad_table, "grad_table", torch.float32, (N, m), like=q),
+        _dev(grad_q, "grad_q", torch.float32, q.shape, like=q) if grad_q is not None else None, _MODES[mode],
+        _stream(q)))
 
 
 class LramLookup(torch.autograd.Function):

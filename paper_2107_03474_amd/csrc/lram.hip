@@ -29,6 +29,7 @@
 #include <cmath>
 #include <stdint.h>
 
+#include <mutex>
 #include <utility>
 
 #include "../../include/lram.h"
@@ -547,6 +548,39 @@ int resolve_mode(int64_t B, int64_t H, int mode, int* resolved) {
 
 constexpr NbrList NO_LIST{nullptr, nullptr, nullptr};
 
+// Workspace of lram_backward_noalloc: one copy per GPU, held from the code
+// object's load until the process ends.  Host code never uses the name as an
+// address (it stands for a host-side shadow): scratch_address() fetches each
+// device's own address once with hipGetSymbolAddress.
+__device__ __align__(256) unsigned char scratch[LRAM_STATIC_SCRATCH_BYTES];
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[MAX_DEVICES] = {};
+
+// Device address of `scratch` on the current device (null and LRAM_EHIP on failure).
+int scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    g_last_hip_error = (int)e;
+    return LRAM_EHIP;
+  }
+  if (dev < 0 || dev >= MAX_DEVICES) return LRAM_EINVAL;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) {
+      g_last_hip_error = (int)e;
+      return LRAM_EHIP;
+    }
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return LRAM_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -653,6 +687,19 @@ int lram_backward(const float* q, int64_t B, int64_t H, const int32_t K[8], cons
   if (int rc = check_saved(nbr_slot, nbr_w, nbr_code, &nl)) return rc;
   return backward_impl(q, B, H, K, table, dtype, N, m, grad_out, grad_table, grad_q, order, order_bytes, nl, mode,
                        workspace, ws_bytes, NB, false, (hipStream_t)stream);
+}
+
+int lram_backward_noalloc(const float* q, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
+                          int64_t N, int32_t m, const float* grad_out, float* grad_table, float* grad_q, int mode,
+                          void* stream) {
+  size_t need = 0;
+  if (int rc = lram_backward_workspace_bytes(B, H, m, mode, &need)) return rc;
+  if (need > LRAM_STATIC_SCRATCH_BYTES) return LRAM_EWORKSPACE;
+  void* ws = nullptr;
+  if (need > 0)
+    if (int rc = scratch_address(&ws)) return rc;
+  return backward_impl(q, B, H, K, table, dtype, N, m, grad_out, grad_table, grad_q, nullptr, 0, NO_LIST, mode, ws,
+                       need > 0 ? LRAM_STATIC_SCRATCH_BYTES : 0, NB, false, (hipStream_t)stream);
 }
 
 int lram_theta_backward(const float* z, int64_t B, int64_t H, const int32_t K[8], const void* table, int dtype,
