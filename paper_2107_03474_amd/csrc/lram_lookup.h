@@ -158,17 +158,20 @@ __device__ __forceinline__ void fwd_accumulate(const WaveLds<KS, NBUF>& W, int b
   }
 }
 
-// Sums the row groups of the wave (xor shuffles) and writes out[l] once.
+// Sums the row groups of the wave (xor shuffles) and writes out[l] once
+// (nothing when !ok: only the store is skipped, so that the row loads are
+// waited for on every path and the next lookup's loads need not wait for
+// this store).
 template <int DT, int M>
 __device__ __forceinline__ void fwd_store(int lane, int64_t l, float (&acc)[FwdGeom<DT, M>::EPL],
-                                          void* __restrict__ out) {
+                                          void* __restrict__ out, bool ok = true) {
   using G = FwdGeom<DT, M>;
   const int rsub = lane / G::LPR, col = lane % G::LPR;
 #pragma unroll
   for (int mask = G::LPR; mask < WAVE; mask <<= 1)
 #pragma unroll
     for (int e = 0; e < G::EPL; ++e) acc[e] += __shfl_xor(acc[e], mask);
-  if (rsub == 0) {
+  if (rsub == 0 && ok) {
     char* ob = reinterpret_cast<char*>(out) + (size_t)l * G::RB + col * G::BPL;
     if constexpr (DT == LRAM_F32) {
       if constexpr (G::EPL == 1)
@@ -184,12 +187,12 @@ __device__ __forceinline__ void fwd_store(int lane, int64_t l, float (&acc)[FwdG
 template <int DT, int M>
 __device__ __forceinline__ void fwd_consume(const WaveLds<NB, 2>& W, int buf, int lane, int64_t l,
                                             const uint32_t (&v)[FwdGeom<DT, M>::NI][FwdGeom<DT, M>::DW],
-                                            void* __restrict__ out) {
+                                            void* __restrict__ out, bool ok = true) {
   float acc[FwdGeom<DT, M>::EPL];
 #pragma unroll
   for (int e = 0; e < FwdGeom<DT, M>::EPL; ++e) acc[e] = 0.0f;
   fwd_accumulate<DT, M, NB>(W, buf, lane, v, acc);
-  fwd_store<DT, M>(lane, l, acc, out);
+  fwd_store<DT, M>(lane, l, acc, out, ok);
 }
 
 // TH: the input is the activation layer's z [L][16] instead of q [L][8]; the
@@ -223,10 +226,9 @@ __global__ void __launch_bounds__(THREADS) k_forward(const float* __restrict__ q
     const int64_t l = ORD ? (int64_t)(uint32_t)__builtin_amdgcn_readlane(my_l, t) : c.base + t;
     // search lookup t+1 while the rows of lookup t are in flight
     if (t + 1 < c.nl) srch.run(FR[t + 1], read_sel(FR[t + 1]), buf ^ 1);
-    if (!ORD || l < P.L) {
-      fwd_consume<DT, M>(W, buf, c.lane, l, v, out);
-      if constexpr (SAVE) srch.save(buf, save, l);
-    }
+    const bool ok = !ORD || l < P.L;
+    fwd_consume<DT, M>(W, buf, c.lane, ok ? l : 0, v, out, ok);
+    if constexpr (SAVE) srch.save(buf, save, l, ok);
     if (t + 1 < c.nl) fwd_issue<DT, M, NB>(tb, W, buf ^ 1, c.lane, v);
   }
 }

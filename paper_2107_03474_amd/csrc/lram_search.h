@@ -599,10 +599,10 @@ struct Search {
     return __popcll(__ballot(real));
   }
 
-  // Writes list `buf` of lookup l to the saved lists (lanes 0..KS-1).
-  __device__ __forceinline__ void save(int buf, const NbrList nl, int64_t l) const {
+  // Writes list `buf` of lookup l to the saved lists (lanes 0..KS-1; nothing when !ok).
+  __device__ __forceinline__ void save(int buf, const NbrList nl, int64_t l, bool ok) const {
     static_assert(KS == NB, "saved lists hold the closest 32");
-    if (lane < KS) {
+    if (lane < KS && ok) {
       const size_t o = (size_t)l * KS + lane;
       const Nbr n = W.nbr[buf][lane];
       nl.slot[o] = n.slot;
