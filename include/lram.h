@@ -120,6 +120,10 @@ int lram_neighbors(const float* q, int64_t B, int64_t H, const int32_t K[8], int
  *   bytes [0, 4)            uint32: how many lookups share their key with a
  *                           neighbour in the order (decides, on the device,
  *                           whether the merged scatter merges)
+ *   bytes [4, 8)            uint32: 0; nonzero if a workgroup of the sort gave
+ *                           up waiting for its predecessors' digit counts (never
+ *                           expected; the order is then not sorted, though every
+ *                           position still names a lookup below L or is skipped)
  *   keys  [L] uint32        at keys_offset: the sorted keys (location, or N for a
  *                           non-finite query)
  *   perm  [L] uint32        at perm_offset: the lookup at each position
@@ -218,7 +222,7 @@ int lram_backward(const float* q, int64_t B, int64_t H, const int32_t K[8], cons
  * sorted and merged scatters is a static array inside the library, one per
  * GPU, LRAM_STATIC_SCRATCH_BYTES long, held from the library's first use on a
  * GPU until the process ends; the call itself allocates nothing.  Up to
- * 5.1 M lookups fit the merged scatter's order (the billion-location
+ * 4.6 M lookups fit the merged scatter's order (the billion-location
  * workload's 4,194,304 included), about 100 K the sorted scatter's pairs;
  * larger calls return LRAM_EWORKSPACE (the atomic mode needs no workspace and
  * takes any size).  Every call on a GPU shares that GPU's array: calls that

@@ -152,31 +152,35 @@ struct Carver {
 };
 
 // Radix-sort buffers for n keys with payloads of type V, ping-ponged between
-// (ka, va) and (kb, vb).
+// (ka, va) and (kb, vb), and the sort's scratch: hdr [SORT_HDR_WORDS] (global
+// digit counts, failure word, gate-count partials) followed by the count
+// states [SORT_PASSES_MAX][tiles + groups][RADIX], all cleared by the sort
+// itself.
 template <typename V>
 struct Radix {
   uint32_t *ka, *kb;
   V *va, *vb;
-  uint32_t *hist, *totals;
+  uint32_t* hdr;
+  uint64_t* state;
   int64_t n;
-  int nblocks;
-  int64_t nh, nbt;
+  int64_t tiles;
+  int64_t states;  // tiles + look-back groups
 };
 
 template <typename V>
 void carve_radix_scratch(int64_t n, Carver& c, Radix<V>* r) {
-  const int nblocks = (int)((n + SORT_TILE - 1) / SORT_TILE);
-  const int64_t nh = (int64_t)RADIX * nblocks;
-  const int64_t nbt = (nh + SCAN_TILE - 1) / SCAN_TILE;
-  char* h = c.take(nh * 4);
-  char* tt = c.take(nbt * 4);
+  const int64_t tiles = (n + SORT_TILE - 1) / SORT_TILE;
+  const int64_t states = tiles + (tiles + LOOKBACK_GROUP - 1) / LOOKBACK_GROUP;
+  // hdr and the states are contiguous (SORT_HDR_WORDS * 4 is a multiple of 256)
+  static_assert((SORT_HDR_WORDS * 4) % 256 == 0, "sort scratch layout");
+  char* h = c.take((size_t)SORT_HDR_WORDS * 4);
+  char* st = c.take((size_t)SORT_PASSES_MAX * states * RADIX * 8);
   if (r) {
-    r->hist = (uint32_t*)h;
-    r->totals = (uint32_t*)tt;
+    r->hdr = (uint32_t*)h;
+    r->state = (uint64_t*)st;
     r->n = n;
-    r->nblocks = nblocks;
-    r->nh = nh;
-    r->nbt = nbt;
+    r->tiles = tiles;
+    r->states = states;
   }
 }
 
@@ -189,36 +193,49 @@ int radix_passes(uint32_t N) {
 // Stable LSD radix sort of the n (key, payload) pairs in (ka, va), keys in
 // [0, N]: the result is in (ka, va) after an even number of passes and in
 // (kb, vb) after an odd one.  IDENT: the payload of element i is i (va is
-// not read).
-template <typename V, bool IDENT>
-int radix_sort(const Radix<V>& r, uint32_t N, hipStream_t s) {
+// not read).  Kernels: clear the scratch, count every pass's digits, then one
+// single-pass scatter per digit.
+template <typename V, bool IDENT, typename S>
+int radix_passes_run(const Radix<V>& r, int passes, hipStream_t s) {
   uint32_t* kin = r.ka;
   uint32_t* kout = r.kb;
   V* vin = r.va;
   V* vout = r.vb;
-  const int passes = radix_passes(N);
   for (int p = 0; p < passes; ++p) {
-    const int shift = p * RADIX_BITS;
-    hipLaunchKernelGGL(k_radix_hist, dim3(r.nblocks), dim3(THREADS), 0, s, kin, r.n, shift, r.hist, r.nblocks);
-    hipLaunchKernelGGL(k_scan_blocks, dim3((unsigned)r.nbt), dim3(THREADS), 0, s, r.hist, r.nh, r.totals);
-    hipLaunchKernelGGL(k_scan_totals, dim3(1), dim3(THREADS), 0, s, r.totals, r.nbt);
-    hipLaunchKernelGGL(k_scan_add, dim3((unsigned)r.nbt), dim3(THREADS), 0, s, r.hist, r.nh, r.totals);
-    if constexpr (IDENT) {
-      if (p == 0)
-        hipLaunchKernelGGL((k_radix_scatter<V, true>), dim3(r.nblocks), dim3(THREADS), 0, s, kin, vin, r.n, shift,
-                           r.hist, r.nblocks, kout, vout);
-      else
-        hipLaunchKernelGGL((k_radix_scatter<V, false>), dim3(r.nblocks), dim3(THREADS), 0, s, kin, vin, r.n, shift,
-                           r.hist, r.nblocks, kout, vout);
-    } else {
-      hipLaunchKernelGGL((k_radix_scatter<V, false>), dim3(r.nblocks), dim3(THREADS), 0, s, kin, vin, r.n, shift,
-                         r.hist, r.nblocks, kout, vout);
-    }
+    S* st = reinterpret_cast<S*>(r.state) + (int64_t)p * r.states * RADIX;
+    const uint32_t* gc = r.hdr + p * RADIX;
+    if (IDENT && p == 0)
+      hipLaunchKernelGGL((k_onesweep<V, IDENT, S>), dim3((unsigned)r.tiles), dim3(THREADS), 0, s,
+                         (const uint32_t*)kin, (const V*)vin, r.n, p * RADIX_BITS, gc, st, r.hdr + SORT_FAIL, kout,
+                         vout);
+    else
+      hipLaunchKernelGGL((k_onesweep<V, false, S>), dim3((unsigned)r.tiles), dim3(THREADS), 0, s,
+                         (const uint32_t*)kin, (const V*)vin, r.n, p * RADIX_BITS, gc, st, r.hdr + SORT_FAIL, kout,
+                         vout);
     if (int rc = launched()) return rc;
     std::swap(kin, kout);
     std::swap(vin, vout);
   }
   return LRAM_OK;
+}
+
+// Stable LSD radix sort of the n (key, payload) pairs in (ka, va), keys in
+// [0, N]: the result is in (ka, va) after an even number of passes and in
+// (kb, vb) after an odd one.  IDENT: the payload of element i is i (va is
+// not read).  Kernels: clear the scratch, count every pass's digits, then one
+// single-pass scatter per digit (32-bit look-back states below 2^30 elements).
+template <typename V, bool IDENT>
+int radix_sort(const Radix<V>& r, uint32_t N, hipStream_t s) {
+  if (r.n <= 0) return LRAM_OK;
+  const int passes = radix_passes(N);
+  const bool small = r.n < SORT_SMALL_STATES;
+  const int64_t words = SORT_HDR_WORDS + (int64_t)passes * r.states * RADIX * (small ? 1 : 2);
+  const int64_t zb = (words + THREADS - 1) / THREADS;
+  hipLaunchKernelGGL(k_zero_words, dim3((unsigned)(zb < 1024 ? zb : 1024)), dim3(THREADS), 0, s, r.hdr, words);
+  hipLaunchKernelGGL(k_digit_hist, dim3((unsigned)(r.tiles < 1024 ? r.tiles : 1024)), dim3(THREADS), 0, s,
+                     (const uint32_t*)r.ka, r.n, passes, r.hdr);
+  if (int rc = launched()) return rc;
+  return small ? radix_passes_run<V, IDENT, uint32_t>(r, passes, s) : radix_passes_run<V, IDENT, uint64_t>(r, passes, s);
 }
 
 // The lookup order of lram_order, which is also the merged scatter's
@@ -306,10 +323,11 @@ int build_order(const float* q, const Params& P, const OrderWs& o, hipStream_t s
   hipLaunchKernelGGL(k_cell_key<TH>, kgrid, dim3(THREADS), 0, s, q, P, r.ka);
   if (int rc = launched()) return rc;
   if (int rc = radix_sort<uint32_t, true>(r, P.N, s)) return rc;
-  hipLaunchKernelGGL(k_fill_u32, dim3(1), dim3(WAVE), 0, s, o.shared, 0u);
   const int64_t cb = (P.L + THREADS - 1) / THREADS;
-  hipLaunchKernelGGL(k_count_shared, dim3((unsigned)(cb < 512 ? cb : 512)), dim3(THREADS), 0, s,
-                     (const uint32_t*)o.sort.ka, P.L, o.shared);
+  hipLaunchKernelGGL(k_count_shared, dim3((unsigned)(cb < 1024 ? cb : 1024)), dim3(THREADS), 0, s,
+                     (const uint32_t*)o.sort.ka, P.L, r.hdr + SORT_COUNT);
+  hipLaunchKernelGGL(k_count_finalize, dim3(1), dim3(WAVE), 0, s, (const uint32_t*)(r.hdr + SORT_COUNT),
+                     (const uint32_t*)(r.hdr + SORT_FAIL), o.shared);
   return launched();
 }
 
@@ -432,7 +450,8 @@ struct BwdSortedLaunch {
     const uint2* vals = odd ? ws.sort.vb : ws.sort.va;
     const int64_t per_block = THREADS / M;
     const unsigned blocks = (unsigned)((ws.groups + per_block - 1) / per_block);
-    hipLaunchKernelGGL((k_segreduce<M>), dim3(blocks), b, 0, s, keys, vals, ws.sort.n, P.N, g, gt, ws.span, ws.edge,
+    hipLaunchKernelGGL((k_segreduce<M>), dim3(blocks), b, 0, s, keys, vals, ws.sort.n, P.N, (uint32_t)P.L, g, gt,
+                       ws.span, ws.edge,
                        ws.flags);
     hipLaunchKernelGGL((k_segfix<M>), dim3(blocks), b, 0, s, keys, ws.sort.n, ws.span, (const float*)ws.edge,
                        (const uint32_t*)ws.flags, ws.groups, gt);

@@ -57,15 +57,12 @@ __global__ void __launch_bounds__(THREADS) k_theta_coords(const float* __restric
   if (s) s[l] = scale;
 }
 
-__global__ void k_fill_u32(uint32_t* __restrict__ p, uint32_t v) {
-  if (threadIdx.x == 0) *p = v;
-}
-
-// *count += number of positions whose sorted key equals a neighbour's (one
-// atomic per workgroup: same-address atomics serialise in memory).
+// Number of positions whose sorted key equals a neighbour's, in COUNT_COPIES
+// partial counters (workgroup b adds into copy b % COUNT_COPIES, cleared, so
+// that few atomics meet on one address); k_count_finalize adds them up.
 __global__ void __launch_bounds__(THREADS) k_count_shared(const uint32_t* __restrict__ keys, int64_t L,
-                                                          uint32_t* __restrict__ count) {
-  __shared__ uint32_t part[WAVES];
+                                                          uint32_t* __restrict__ copies) {
+  __shared__ uint32_t wsum[WAVES];
   uint32_t c = 0;
   for (int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x; i < L; i += (int64_t)gridDim.x * THREADS) {
     const uint32_t k = keys[i];
@@ -73,13 +70,25 @@ __global__ void __launch_bounds__(THREADS) k_count_shared(const uint32_t* __rest
   }
 #pragma unroll
   for (int mask = 1; mask < WAVE; mask <<= 1) c += __shfl_xor(c, mask);
-  if (threadIdx.x % WAVE == 0) part[threadIdx.x / WAVE] = c;
+  if (threadIdx.x % WAVE == 0) wsum[threadIdx.x / WAVE] = c;
   __syncthreads();
   if (threadIdx.x == 0) {
-    uint32_t t = 0;
+    const uint32_t t = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+    if (t) atomicAdd(copies + blockIdx.x % COUNT_COPIES, t);
+  }
+}
+
+// count[0] = the sum of the partial counters, count[1] = the sort's failure
+// word (one wave).
+__global__ void k_count_finalize(const uint32_t* __restrict__ copies, const uint32_t* __restrict__ sort_fail,
+                                 uint32_t* __restrict__ count) {
+  uint32_t s = 0;
+  for (int i = threadIdx.x; i < COUNT_COPIES; i += WAVE) s += copies[i];
 #pragma unroll
-    for (int w = 0; w < WAVES; ++w) t += part[w];
-    if (t) atomicAdd(count, t);
+  for (int mask = 1; mask < WAVE; mask <<= 1) s += __shfl_xor(s, mask);
+  if (threadIdx.x == 0) {
+    count[0] = s;
+    count[1] = *sort_fail;
   }
 }
 
