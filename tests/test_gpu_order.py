@@ -7,7 +7,7 @@ backward calls that take it.
     tie by an ulp), N for a non-finite query; keys sorted,
     positions a permutation, equal keys in lookup order (the sort is stable);
     the gate count equals the number of positions whose key equals a
-    neighbour's;
+    neighbour's; the sort's failure word is 0;
   * the same points given as q - K and q + 3K (exact in fp32 on a 2^-10 grid)
     give the same keys, positions and gate count, and the merged backward the
     same gradients (Sec. 2.2: the torus periods);
@@ -54,6 +54,7 @@ def _check_order(q_np, K, buf):
     L = q_np.shape[0]
     N = int(np.prod(K))
     cnt, keys, perm = _view(buf, L)
+    assert int(buf[4:8].view(torch.int32).item()) == 0      # the sort's failure word
     assert np.all(np.diff(keys) >= 0)
     assert np.array_equal(np.sort(perm), np.arange(L))
     same = np.diff(keys) == 0
@@ -102,6 +103,50 @@ def test_order_ragged_sizes():
         buf = lram.order(q, K8)
         torch.cuda.synchronize()
         _check_order(q_np, K8, buf)
+
+
+def test_order_several_lookback_groups():
+    """Sizes whose tiles (4,096 lookups) span several look-back groups of 32
+    tiles, with a ragged last tile and group: 300,007 lookups against the
+    oracle; 4,194,309 (33 groups, as at the billion-location workload plus a
+    ragged tile) on sort properties and against the closest points that
+    lram_neighbors lists first."""
+    rng = np.random.default_rng(7)
+    q_np = _clustered(300007, 3)
+    q_np[5] = np.nan
+    q = torch.from_numpy(q_np).to(DEV)
+    buf = lram.order(q, K8)
+    torch.cuda.synchronize()
+    _check_order(q_np, K8, buf)
+    K = (14,) * 8
+    L = 4194309
+    q_np = (rng.random((L, 8)) * 14).astype(np.float32)
+    centres = rng.random((2000, 8)) * 14               # half the lookups around 2,000 points: shared cells
+    q_np[: L // 2] = np.mod(centres[rng.integers(0, 2000, L // 2)] + 0.02 * rng.standard_normal((L // 2, 8)),
+                            14).astype(np.float32)
+    q = torch.from_numpy(q_np).to(DEV)
+    buf = lram.order(q, K)
+    slot, _, d2 = lram.neighbors(q, K)
+    torch.cuda.synchronize()
+    assert int(buf[4:8].view(torch.int32).item()) == 0
+    cnt, keys, perm = _view(buf, L)
+    assert np.all(np.diff(keys) >= 0)
+    assert np.array_equal(np.sort(perm), np.arange(L))
+    same = np.diff(keys) == 0
+    assert np.all(np.diff(perm)[same] > 0)
+    shared = np.zeros(L, bool)
+    shared[1:] |= same
+    shared[:-1] |= same
+    assert cnt == int(shared.sum()) and cnt > L // 4
+    key_of = np.empty(L, np.int64)
+    key_of[perm] = keys
+    s0 = slot[:, 0].cpu().numpy()
+    off = np.nonzero(key_of != s0)[0]
+    if off.size:
+        sl, dd = slot[off].cpu().numpy(), d2[off].cpu().numpy()
+        near = dd <= dd[:, :1] * np.float32(1 + 2 ** -20)
+        assert np.all(((sl == key_of[off][:, None]) & near).any(axis=1))
+        assert int((dd[:, 0] != dd[:, 1]).sum()) <= max(2, L // 10000)
 
 
 def test_order_and_merged_backward_see_through_the_wrap():

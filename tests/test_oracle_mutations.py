@@ -135,7 +135,10 @@ def _variable_k_battery():
 def _subnetwork_battery():
     return [
         ("identity dense parts reduce to theta", subt.test_identity_dense_parts_reduce_to_theta),
-        ("gradients against finite differences", subt.test_gradients_match_directional_finite_differences),
+        ("training normalisation closed forms", subt.test_training_normalisation_closed_forms),
+        ("gradients against finite differences", lambda: subt.test_gradients_match_directional_finite_differences(False)),
+        ("training gradients against finite differences",
+         lambda: subt.test_gradients_match_directional_finite_differences(True)),
     ]
 
 
@@ -206,12 +209,26 @@ C_VARIABLE_K_MUTANTS = {
 PY_SUBNETWORK_MUTANTS = {
     # Sec. 3.1: y = W2 theta(BN(W1 x + b1)) + b2
     "first dense layer transposed": ("forward", 'pre = x @ p["W1"].T + p["b1"]', 'pre = x @ p["W1"] + p["b1"]'),
-    "batch norm without the square root": ("forward", 'inv = 1.0 / np.sqrt(p["var"] + p["eps"])',
-                                           'inv = 1.0 / (p["var"] + p["eps"])'),
-    "gamma gradient from the unnormalised features": ("backward", 'norm = (st["pre"] - p["mu"]) * st["inv"]',
-                                                      'norm = st["pre"] - p["mu"]'),
-    "pre-activation gradient without the normalisation": ("backward", 'dpre = dz * p["gamma"] * st["inv"]',
-                                                          'dpre = dz * p["gamma"]'),
+    "batch norm without the square root": ("_normalise", 'inv = 1.0 / np.sqrt(var + p["eps"])',
+                                           'inv = 1.0 / (var + p["eps"])'),
+    "gamma gradient from the unnormalised features": ("backward", 'g["gamma"] = (dz * st["xhat"]).sum(0)',
+                                                      'g["gamma"] = (dz * (st["pre"] - st["mu"])).sum(0)'),
+    "pre-activation gradient without the normalisation": ("backward", 'dpre = dxhat * st["inv"]',
+                                                          'dpre = dxhat'),
+    # Sec. 3.1 / 4.1 in training: batch statistics, biased variance, and the
+    # gradient through them
+    "batch variance unbiased": ("_normalise", "var = ((pre - mu) ** 2).mean(0)",
+                                "var = ((pre - mu) ** 2).sum(0) / (pre.shape[0] - 1)"),
+    "batch mean from the running mean": ("_normalise", "mu = pre.mean(0)", 'mu = p["mu"]'),
+    "training gradient without the batch statistics": (
+        "backward", 'dpre = st["inv"] * (dxhat - dxhat.mean(0) - st["xhat"] * (dxhat * st["xhat"]).mean(0))',
+        'dpre = st["inv"] * dxhat'),
+    "training gradient without the variance term": (
+        "backward", 'dpre = st["inv"] * (dxhat - dxhat.mean(0) - st["xhat"] * (dxhat * st["xhat"]).mean(0))',
+        'dpre = st["inv"] * (dxhat - dxhat.mean(0))'),
+    "training gradient without the mean term": (
+        "backward", 'dpre = st["inv"] * (dxhat - dxhat.mean(0) - st["xhat"] * (dxhat * st["xhat"]).mean(0))',
+        'dpre = st["inv"] * (dxhat - st["xhat"] * (dxhat * st["xhat"]).mean(0))'),
 }
 
 PY_THETA_MUTANTS = {

@@ -1,9 +1,13 @@
 """Pins of the oracle's memory subnetwork (Sec. 3.1): it reduces to the pinned
-activation layer when the dense parts are identities, and its gradients match
+activation layer when the dense parts are identities; in training form the
+normalised features have zero batch mean and a batch second moment of
+var / (var + eps) (biased variance), the output does not depend on b1 (the
+batch mean removes it) and the b1 gradient vanishes; and its gradients match
 directional finite differences of an independent fp64 evaluation with the
-neighbour selection held fixed.
+neighbour selection held fixed, in inference and in training form.
 """
 import numpy as np
+import pytest
 
 import oracle
 from oracle import subnetwork as sub
@@ -38,12 +42,39 @@ def test_identity_dense_parts_reduce_to_theta():
     np.testing.assert_allclose(y[:, 16:], th[:, 1, :16], rtol=1e-13)
 
 
-def _fixed_eval(x, p, table, st):
+def test_training_normalisation_closed_forms():
+    rng = np.random.default_rng(3)
+    w, T = 32, 48
+    table = rng.standard_normal((int(np.prod(K)), 64))
+    p = _params(w, rng, scale=3.0)
+    x = rng.standard_normal((T, w))
+    y, st = sub.forward(x, p, K, table, training=True)
+    pre = st["pre"]
+    c = pre - pre.sum(0) / T
+    var = np.einsum("tw,tw->w", c, c) / T
+    np.testing.assert_allclose(st["xhat"].sum(0) / T, 0.0, atol=1e-13)
+    np.testing.assert_allclose(np.einsum("tw,tw->w", st["xhat"], st["xhat"]) / T, var / (var + p["eps"]),
+                               rtol=1e-12)
+    # the batch mean removes any shift of the pre-activations
+    p2 = dict(p)
+    p2["b1"] = p["b1"] + rng.standard_normal(w)
+    y2, _ = sub.forward(x, p2, K, table, training=True)
+    np.testing.assert_allclose(y2, y, rtol=1e-9, atol=1e-12)
+    g = sub.backward(rng.standard_normal(y.shape), p, K, table, st)
+    assert np.abs(g["b1"]).max() <= 1e-10 * np.abs(g["beta"]).max()
+
+
+def _fixed_eval(x, p, table, st, training=False):
     """fp64 forward with the lattice points of every lookup fixed (the lists in st)."""
     T, w = x.shape
     h = w // 16
     pre = x @ p["W1"].T + p["b1"]
-    z = (((pre - p["mu"]) / np.sqrt(p["var"] + p["eps"])) * p["gamma"] + p["beta"]).reshape(T, h, 16)
+    if training:
+        mean = pre.sum(0) / T
+        var = ((pre - mean) ** 2).sum(0) / T
+    else:
+        mean, var = p["mu"], p["var"]
+    z = (((pre - mean) / np.sqrt(var + p["eps"])) * p["gamma"] + p["beta"]).reshape(T, h, 16)
     z0 = st["z"]
     c = np.asarray(K, np.float64) / (2 * np.pi)
     a, b = z[..., 0::2], z[..., 1::2]
@@ -58,38 +89,41 @@ def _fixed_eval(x, p, table, st):
     return th @ p["W2"].T + p["b2"]
 
 
-def test_gradients_match_directional_finite_differences():
+@pytest.mark.parametrize("training", [False, True])
+def test_gradients_match_directional_finite_differences(training):
     rng = np.random.default_rng(2)
     w, T = 32, 40
     table = rng.standard_normal((int(np.prod(K)), 64))
     p = _params(w, rng, scale=3.0)
     x = rng.standard_normal((T, w))
-    y, st = sub.forward(x, p, K, table)
+    y, st = sub.forward(x, p, K, table, training=training)
     dy = rng.standard_normal(y.shape)
     g = sub.backward(dy, p, K, table, st)
     # the oracle's forward rounds q to fp32; evaluate the fixed-selection
     # function around the same base point (x_lat from the oracle's lists)
-    st["z"] = st["z"].astype(np.float32).astype(np.float64)
+    st["z"] = st["zq"].astype(np.float64)
     h = 1e-6
     for name in ("x", "W1", "b1", "gamma", "beta", "W2", "b2"):
         for trial in range(3):
             d = rng.standard_normal(x.shape if name == "x" else p[name].shape)
             if name == "x":
-                fp = _fixed_eval(x + h * d, p, table, st)
-                fm = _fixed_eval(x - h * d, p, table, st)
+                fp = _fixed_eval(x + h * d, p, table, st, training)
+                fm = _fixed_eval(x - h * d, p, table, st, training)
                 an = np.sum(g["x"] * d)
             else:
                 pp, pm = dict(p), dict(p)
                 pp[name] = p[name] + h * d
                 pm[name] = p[name] - h * d
-                fp = _fixed_eval(x, pp, table, st)
-                fm = _fixed_eval(x, pm, table, st)
+                fp = _fixed_eval(x, pp, table, st, training)
+                fm = _fixed_eval(x, pm, table, st, training)
                 an = np.sum(g[name] * d)
             fd = np.sum(dy * (fp - fm)) / (2 * h)
-            np.testing.assert_allclose(an, fd, rtol=2e-5, err_msg=name)
+            # atol: the b1 derivative vanishes in training form, where the
+            # difference quotient is rounding noise (~1e-10)
+            np.testing.assert_allclose(an, fd, rtol=2e-5, atol=1e-8, err_msg=name)
     # table: the slice is linear in it
     uniq, acc = g["table"]
     probe = rng.standard_normal(table.shape)
     tp = table + probe
-    yp, _ = sub.forward(x, p, K, tp)
+    yp, _ = sub.forward(x, p, K, tp, training=training)
     np.testing.assert_allclose(np.sum(dy * (yp - y)), np.sum(acc * probe[uniq]), rtol=1e-10)
