@@ -15,7 +15,11 @@ and every classification near r^2 = 8 is re-derived in exact rational
 arithmetic.
 
 Output (``e8_candidates.inc``):
-  * the STRICT list  -- dist(p, F)^2 < 8 (the paper's 232 points);
+  * the STRICT list  -- dist(p, F)^2 < 8 (the paper's 232 points), in
+    ascending order of that distance, and E8_FAST / E8_FAST_BOUND: the first
+    E8_FAST of them and the exact distance^2 from F of every later one, at
+    least E8_FAST_BOUND (a query in F whose k-th closest point among the
+    first E8_FAST lies below that bound takes its closest k from them);
   * the BOUNDARY list -- dist(p, F)^2 == 8 exactly.  These never lie in the open
     support of a query inside F, but a query whose reduction lands a rounding
     error outside F, or whose fp32 distance rounds below 8, can see them; the
@@ -32,6 +36,9 @@ import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 OUT = os.path.join(HERE, "e8_candidates.inc")
+
+
+FAST = 192  # three candidates per lane of a 64-lane wave
 
 
 def lattice_points(max_norm: int) -> np.ndarray:
@@ -130,12 +137,15 @@ def main(write: bool = True) -> dict:
             continue
         ex = exact_dist2(P[i], sets[i])
         if ex < 8:
-            strict.append(P[i])
+            strict.append((ex, P[i]))
         elif ex == 8:
             boundary.append(P[i])
         else:
             above.append(float(ex))
-    strict = sorted(strict, key=lambda v: (int((v * v).sum()), tuple(-v)))
+    strict = sorted(strict, key=lambda e: (e[0], int((e[1] * e[1]).sum()), tuple(-e[1])))
+    strict_d2 = [e[0] for e in strict]
+    strict = [e[1] for e in strict]
+    fast_bound = strict_d2[FAST] if FAST < len(strict) else Fraction(8)
     boundary = sorted(boundary, key=lambda v: (int((v * v).sum()), tuple(-v)))
     gap = min(above) - 8.0
     norms = {}
@@ -143,7 +153,7 @@ def main(write: bool = True) -> dict:
         norms[int((v * v).sum())] = norms.get(int((v * v).sum()), 0) + 1
     allpts = np.array(strict + boundary)
     info = dict(strict=np.array(strict), boundary=np.array(boundary), gap=gap, norms=norms,
-                cmin=int(allpts.min()), cmax=int(allpts.max()))
+                cmin=int(allpts.min()), cmax=int(allpts.max()), strict_d2=strict_d2, fast_bound=fast_bound)
     if write:
         with open(OUT, "w") as f:
             f.write("// Generated by gen_e8_candidates.py -- do not edit.\n")
@@ -153,6 +163,8 @@ def main(write: bool = True) -> dict:
             f.write("#pragma once\n")
             f.write("#define E8_NSTRICT %d\n#define E8_NBOUNDARY %d\n" % (len(strict), len(boundary)))
             f.write("#define E8_CAND_MIN %d\n#define E8_CAND_MAX %d\n" % (info["cmin"], info["cmax"]))
+            f.write("// Strict points FAST.. lie at distance^2 >= %s from F.\n" % fast_bound)
+            f.write("#define E8_FAST %d\n#define E8_FAST_BOUND %.9gf\n" % (FAST, float(fast_bound)))
             for name, lst in (("E8_STRICT_INIT", strict), ("E8_BOUNDARY_INIT", boundary)):
                 f.write("#define %s { \\\n" % name)
                 for v in lst:

@@ -499,42 +499,65 @@ struct Search {
     if (sel.misc & 0x100u) {
       build_tables(F, sel.misc);
       wave_lds_sync();
-      uint32_t key[NS_STRICT];
-#pragma unroll
-      for (int k = 0; k < NS_STRICT; ++k)
-        key[k] = (lane + WAVE * k < E8_NSTRICT) ? __float_as_uint(cand_d2(S.qt, lo[k], hi[k], sel)) : KEY_INF;
       uint32_t thr = KEY_8, tie_key = KEY_INF;
       int need = 0;
       bool suspect = true;
-      if constexpr (KS != KALL) count = threshold_k_hist<NS_STRICT>(key, W.hist, lane, KS, thr, tie_key, need, suspect);
-      if (!suspect) {
-        emit<NS_STRICT>(key, thr, tie_key, need, sel, F, buf);
-      } else {
-        // rare: rescan together with the points at distance exactly sqrt(8) from F
-        uint32_t key7[NS_ALL];
+      bool fast = false;
+      // lists of up to 32: scan the E8_FAST candidates nearest to F first;
+      // when the ks-th closest of them is below KEY_FAST none of the others
+      // can be among the closest ks (nearly every query)
+      uint32_t key3[NS_FAST];
+      if constexpr (KS <= NB) {
 #pragma unroll
-        for (int k = 0; k < NS_STRICT; ++k) key7[k] = key[k];
-        if constexpr (NB_REG == NS_BOUND) {
+        for (int k = 0; k < NS_FAST; ++k) key3[k] = __float_as_uint(cand_d2(S.qt, lo[k], hi[k], sel));
+        count = threshold_k_hist<NS_FAST>(key3, W.hist, lane, KS, thr, tie_key, need, suspect);
+        fast = count == KS && !suspect && (tie_key != KEY_INF ? tie_key < KEY_FAST : thr <= KEY_FAST);
+        if (fast) emit<NS_FAST>(key3, thr, tie_key, need, sel, F, buf);
+      }
+      if (!fast) {
+        uint32_t key[NS_STRICT];
 #pragma unroll
-          for (int k = 0; k < NS_BOUND; ++k)
-            key7[NS_STRICT + k] = (lane + WAVE * k < E8_NBOUNDARY) ? __float_as_uint(cand_d2(S.qt, blo[k], bhi[k], sel))
-                                                                   : KEY_INF;
-        } else {
-#pragma unroll 1
-          for (int k = 0; k < NS_BOUND; ++k) {
-            uint32_t l, h;
-            const bool okb = load_candidate<1>(lane + WAVE * k, wbyte, l, h);
-            key7[NS_STRICT + k] = okb ? __float_as_uint(cand_d2(S.qt, l, h, sel)) : KEY_INF;
-          }
+        for (int k = 0; k < NS_STRICT; ++k) {
+          if (KS <= NB && k < NS_FAST)
+            key[k] = key3[k];
+          else
+            key[k] = (lane + WAVE * k < E8_NSTRICT) ? __float_as_uint(cand_d2(S.qt, lo[k], hi[k], sel)) : KEY_INF;
         }
-        if constexpr (KS == KALL) {
-          // untruncated: every candidate whose recipe distance is below 8
-          count = min(count_below(key7, KEY_8), KS);
-          emit<NS_ALL>(key7, KEY_8, KEY_INF, 0, sel, F, buf);
+        thr = KEY_8;
+        tie_key = KEY_INF;
+        need = 0;
+        suspect = true;
+        if constexpr (KS != KALL)
+          count = threshold_k_hist<NS_STRICT>(key, W.hist, lane, KS, thr, tie_key, need, suspect);
+        if (!suspect) {
+          emit<NS_STRICT>(key, thr, tie_key, need, sel, F, buf);
         } else {
-          bool suspect7;
-          count = threshold_k<NS_ALL>(key7, KS, thr, tie_key, need, suspect7);
-          emit<NS_ALL>(key7, thr, tie_key, need, sel, F, buf);
+          // rare: rescan together with the points at distance exactly sqrt(8) from F
+          uint32_t key7[NS_ALL];
+#pragma unroll
+          for (int k = 0; k < NS_STRICT; ++k) key7[k] = key[k];
+          if constexpr (NB_REG == NS_BOUND) {
+#pragma unroll
+            for (int k = 0; k < NS_BOUND; ++k)
+              key7[NS_STRICT + k] =
+                  (lane + WAVE * k < E8_NBOUNDARY) ? __float_as_uint(cand_d2(S.qt, blo[k], bhi[k], sel)) : KEY_INF;
+          } else {
+#pragma unroll 1
+            for (int k = 0; k < NS_BOUND; ++k) {
+              uint32_t l, h;
+              const bool okb = load_candidate<1>(lane + WAVE * k, wbyte, l, h);
+              key7[NS_STRICT + k] = okb ? __float_as_uint(cand_d2(S.qt, l, h, sel)) : KEY_INF;
+            }
+          }
+          if constexpr (KS == KALL) {
+            // untruncated: every candidate whose recipe distance is below 8
+            count = min(count_below(key7, KEY_8), KS);
+            emit<NS_ALL>(key7, KEY_8, KEY_INF, 0, sel, F, buf);
+          } else {
+            bool suspect7;
+            count = threshold_k<NS_ALL>(key7, KS, thr, tie_key, need, suspect7);
+            emit<NS_ALL>(key7, thr, tie_key, need, sel, F, buf);
+          }
         }
       }
       wave_lds_sync();

@@ -34,6 +34,17 @@ def _read_lists():
 STRICT, BOUNDARY = _read_lists()
 
 
+def _read_fast():
+    txt = open(INC).read()
+    n = int(re.search(r"#define E8_FAST (\d+)", txt).group(1))
+    bound = float(re.search(r"#define E8_FAST_BOUND ([\d.]+)f", txt).group(1))
+    return n, bound
+
+
+FAST, FAST_BOUND = _read_fast()
+FAST_LIMIT = np.float32(FAST_BOUND - 2.0 ** -7)   # the kernels' margin
+
+
 def _d8_round(y):
     r = np.rint(y)
     bad = (r.sum(1) % 2) != 0
@@ -76,7 +87,9 @@ def _recipe(x, k):
     return d
 
 
-def model_neighbors(q, K):
+def model_neighbors(q, K, fast=False):
+    """fast: first the FAST candidates nearest to F; their closest 32 stand
+    when the 32nd is below the bound every later candidate respects."""
     K = np.asarray(K)
     x = np.fmod(np.float32(2) * q, (2 * K).astype(np.float32)).astype(np.float32)
     c, r, s = _reduce(x)
@@ -89,8 +102,15 @@ def model_neighbors(q, K):
     dS = _recipe(x, kS)
     out_slots = np.full((q.shape[0], 32), -1, np.int64)
     suspects = 0
+    fallbacks = 0
     for l in range(q.shape[0]):
         d, k = dS[l], kS[l]
+        if fast:
+            dF = np.sort(d[:FAST])
+            if dF.size >= 32 and dF[31] < FAST_LIMIT:
+                d, k = d[:FAST], k[:FAST]
+            else:
+                fallbacks += 1
         keep = d < np.float32(8)
         n8 = keep.sum()
         dd = np.sort(d[keep])
@@ -107,6 +127,8 @@ def model_neighbors(q, K):
         bits = d.view(np.uint32).astype(np.int64)
         order = np.lexsort(tuple(k[:, i] for i in range(7, -1, -1)) + (slot, bits))[:32]
         out_slots[l, :order.size] = slot[order]
+    if fast:
+        return out_slots, suspects, fallbacks
     return out_slots, suspects
 
 
@@ -156,3 +178,38 @@ def test_model_special_points():
     nb = oracle.neighbors(q, K)
     np.testing.assert_array_equal(slots, nb["slot"])
     assert suspects >= 3
+
+
+def test_fast_set_bound_is_exact():
+    """Every strict candidate after the first E8_FAST lies at least
+    E8_FAST_BOUND from F (exact distances from the generator's quadratic
+    programs), and the first E8_FAST are the nearest to F."""
+    import importlib.util
+    spec = importlib.util.spec_from_file_location(
+        "gen", os.path.join(ROOT, "paper_2107_03474_amd", "csrc", "gen_e8_candidates.py"))
+    gen = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(gen)
+    d2, sets = gen.project_all(STRICT)
+    exact = [gen.exact_dist2(STRICT[i], sets[i]) for i in range(STRICT.shape[0])]
+    assert FAST == 192 and FAST % 64 == 0
+    assert min(exact[FAST:]) >= FAST_BOUND and max(exact[:FAST]) <= min(exact[FAST:])
+    assert all(exact[i] <= exact[i + 1] for i in range(len(exact) - 1))
+
+
+@pytest.mark.parametrize("K", [(4,) * 8, (14,) * 8, (2, 4, 6, 8, 2, 4, 6, 8)])
+def test_fast_set_model_matches_oracle(K):
+    """The fast-set rule of the kernels' search gives the oracle's lists, on
+    random, clustered, dyadic and special queries; the full scan is needed for
+    a small share only."""
+    rng = np.random.default_rng(123)
+    n = 3000
+    Kf = np.asarray(K, np.float64)
+    q = rng.random((n, 8)) * Kf
+    q[:500] = np.mod(np.floor(q[:500] * 16) / 16, Kf)        # dyadic grid: exact ties
+    q[500:600] = np.floor(q[500:600])                       # lattice points and deep holes
+    q[600:700] = np.floor(q[600:700]) + 1e-6 * rng.standard_normal((100, 8))
+    q = q.astype(np.float32)
+    got, _, fallbacks = model_neighbors(q, K, fast=True)
+    nb = oracle.neighbors(q, K)
+    np.testing.assert_array_equal(got, nb["slot"])
+    assert fallbacks < n // 4
