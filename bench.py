@@ -682,43 +682,63 @@ def time_small_graph(torch, lram, W, log, reps=200):
 
 def time_training(torch, lram, W, log, batches=16):
     """The utilisation table's analogue and the optimiser step at the paper's
-    memory sizes (2^18, 2^20, 2^22 locations of m = 64 fp32): access share and
-    KL over `batches` synthetic batches of 8192 x 32 lookups (the queries of
-    the bench workload's Zipf/uniform mix on each torus), then one backward +
-    sparse Adam step per batch; Adam time and its HBM rate (grad scan + the
-    touched rows' moments, values and cleared gradient)."""
+    memory sizes (2^18, 2^20, 2^22 locations of m = 64 fp32) and at 2^26:
+    access share and KL over `batches` synthetic batches of 8192 x 32 lookups
+    (the queries of the bench workload's Zipf/uniform mix on each torus; one
+    batch at 2^26), then one backward + sparse Adam step per batch, twice:
+    the full-scan step, and the touched-row step (flags from mark_touched for
+    the batch, then the step on the flagged rows) on a copy of the same table,
+    moments and gradient.  Adam times and the full step's HBM rate (grad scan +
+    the touched rows' moments, values and cleared gradient)."""
     out = {}
-    for name, K in (("2^18", (4, 4, 4, 4, 4, 4, 8, 8)), ("2^20", (4, 4, 4, 4, 8, 8, 8, 8)),
-                    ("2^22", (4, 4, 8, 8, 8, 8, 8, 8))):
+    for name, K, nb in (("2^18", (4, 4, 4, 4, 4, 4, 8, 8), batches), ("2^20", (4, 4, 4, 4, 8, 8, 8, 8), batches),
+                        ("2^22", (4, 4, 8, 8, 8, 8, 8, 8), batches), ("2^26", (8, 8, 8, 8, 8, 8, 16, 16), 1)):
         N = int(np.prod(K))
         wl = W.Workload("stats", K, 64, "f32", 8192, 32, "zipf_mix", True, gmm_sigma=0.3, zipf_centres=4096,
                         zipf_s=1.1)
         table = torch.randn((N, 64), device="cuda") * 0.02
+        table2 = table.clone()
         opt = lram.SparseAdam(table, lr=1e-3)
+        opt2 = lram.SparseAdam(table2, lr=1e-3)
         gtab = torch.zeros((N, 64), dtype=torch.float32, device="cuda")
         hist = torch.zeros(N, dtype=torch.float32, device="cuda")
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-        adam_ms, touched = 0.0, 0
-        for b in range(batches):
+        flags = torch.zeros(N, dtype=torch.uint8, device="cuda")
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        adam_ms = touched_ms = mark_ms = 0.0
+        touched = 0
+        for b in range(nb):
             q = torch.from_numpy(W.queries(wl, seed=100 + b)).to("cuda")
             lram.access_histogram(q, K, hist)
             G = torch.randn((wl.B, wl.H, 64), device="cuda")
             lram.backward(q, table, K, G, grad_table=gtab, want_grad_q=False)
-            if b == batches - 1:
+            gtab2 = gtab.clone()
+            if b == nb - 1:
                 touched = int((gtab != 0).any(1).sum().item())
+            torch.cuda.synchronize()
             ev[0].record()
             opt.step(gtab)
             ev[1].record()
+            lram.mark_touched(q, K, flags)
+            ev[2].record()
+            opt2.step(gtab2, flags)
+            ev[3].record()
             torch.cuda.synchronize()
-            adam_ms += ev[0].elapsed_time(ev[1]) / batches
+            adam_ms += ev[0].elapsed_time(ev[1]) / nb
+            mark_ms += ev[1].elapsed_time(ev[2]) / nb
+            touched_ms += ev[2].elapsed_time(ev[3]) / nb
+            del gtab2
+        same = bool(torch.equal(table, table2))
         st = lram.access_stats(hist)
         adam_bytes = N * 64 * 4 + touched * 64 * 4 * 7
-        out[name] = {"locations": N, "K": list(K), "lookups": batches * wl.L, "used": st["used"], "kl": st["kl"],
+        out[name] = {"locations": N, "K": list(K), "lookups": nb * wl.L, "used": st["used"], "kl": st["kl"],
                      "adam_ms": adam_ms, "adam_touched_rows": touched,
-                     "adam_GBps": adam_bytes / (adam_ms * 1e-3) / 1e9}
-        log("memory %s: used %.4f, KL %.3f over %d lookups; Adam step %.3f ms (%d touched rows, %.0f GB/s)" % (
-            name, st["used"], st["kl"], batches * wl.L, adam_ms, touched, out[name]["adam_GBps"]))
-        del table, opt, gtab, hist
+                     "adam_GBps": adam_bytes / (adam_ms * 1e-3) / 1e9,
+                     "adam_touched_step_ms": touched_ms, "mark_touched_ms": mark_ms, "touched_step_identical": same}
+        log("memory %s: used %.4f, KL %.3f over %d lookups; Adam step %.3f ms full scan (%d touched rows, %.0f GB/s), "
+            "%.3f ms on the flagged rows (+ %.3f ms marking them), identical %s" % (
+                name, st["used"], st["kl"], nb * wl.L, adam_ms, touched, out[name]["adam_GBps"], touched_ms, mark_ms,
+                same))
+        del table, table2, opt, opt2, gtab, hist, flags
         torch.cuda.empty_cache()
     return out
 

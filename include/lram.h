@@ -264,6 +264,25 @@ int lram_sparse_adam(void* table, int dtype, int64_t N, int32_t m, float* grad, 
                      int64_t step, double lr, double beta1, double beta2, double eps, void* stream);
 
 /*
+ * lram_mark_touched -- touched[s] = 1 (uint8 [N], device) for every location s
+ * in the closest-32 list of every lookup of q (Sec. 2.6): the rows that
+ * lram_backward of these lookups writes.  Other entries are left as they are
+ * (the caller clears the array once; lram_sparse_adam_touched clears what it
+ * uses).
+ *
+ * lram_sparse_adam_touched -- lram_sparse_adam on the rows whose touched flag
+ * is set, in the same arithmetic (a flagged row whose gradient row is
+ * identically zero keeps value and moments); the flags of [0, N) are cleared.
+ * The step reads the N flag bytes and the flagged rows only, so its cost
+ * follows the touched rows rather than the table size (Sec. 3.2: the memory's
+ * rows are a sparse parameter; most of a large table is untouched by a step).
+ */
+int lram_mark_touched(const float* q, int64_t B, int64_t H, const int32_t K[8], uint8_t* touched, void* stream);
+int lram_sparse_adam_touched(void* table, int dtype, int64_t N, int32_t m, float* grad, float* exp_avg,
+                             float* exp_avg_sq, uint8_t* touched, int64_t step, double lr, double beta1, double beta2,
+                             double eps, void* stream);
+
+/*
  * Variable k and the untruncated lookup (Sec. 2.2 and 2.5: the sum over every
  * lattice point in the support; Sec. 2.6: the truncation to the closest k,
  * whose k = 32 is what every other entry point uses).  k is 16, 32, 64 or

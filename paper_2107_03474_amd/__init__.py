@@ -25,6 +25,7 @@ __all__ = ["neighbors", "forward", "backward", "backward_workspace_bytes", "look
            "SCATTER_MERGED", "SCATTER_AUTO", "resolved_mode", "NB",
            "theta_coords", "theta_forward", "theta_backward", "ThetaLookup", "theta", "ALL", "MAX_SUPPORT",
            "list_width", "access_histogram", "access_stats", "sparse_adam", "SparseAdam", "Lists", "new_lists",
+           "mark_touched",
            "order", "order_layout", "order_view", "backward_noalloc"]
 
 NB = 32
@@ -92,6 +93,11 @@ def load():
             lib.lram_sparse_adam.argtypes = [P, I, I64, I32, P, P, P, I64, ctypes.c_double, ctypes.c_double,
                                              ctypes.c_double, ctypes.c_double, P]
             lib.lram_sparse_adam.restype = I
+            lib.lram_mark_touched.argtypes = [P, I64, I64, P, P, P]
+            lib.lram_mark_touched.restype = I
+            lib.lram_sparse_adam_touched.argtypes = [P, I, I64, I32, P, P, P, P, I64, ctypes.c_double,
+                                                     ctypes.c_double, ctypes.c_double, ctypes.c_double, P]
+            lib.lram_sparse_adam_touched.restype = I
             lib.lram_theta_coords.argtypes = [P, I64, I64, P, P, P, P]
             lib.lram_theta_coords.restype = I
             lib.lram_theta_forward.argtypes = [P, I64, I64, P, P, I, I64, I32, P, P]
@@ -473,18 +479,35 @@ def access_stats(hist: torch.Tensor) -> dict:
     return {"used": v[0], "kl": v[1], "total": v[2], "count": int(round(v[3]))}
 
 
+def mark_touched(q: torch.Tensor, K: Sequence[int], touched: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """touched [N] uint8: set to 1 at every location in the closest-32 lists of
+    the lookups of q (allocated zeroed if None; other entries unchanged)."""
+    lib = load()
+    B, H = _bh(q)
+    N = int(np.prod([int(k) for k in K]))
+    if touched is None:
+        touched = torch.zeros(N, dtype=torch.uint8, device=q.device)
+    _check(lib.lram_mark_touched(_dev(q, "q", torch.float32), B, H, _K(K),
+                                 _dev(touched, "touched", torch.uint8, (N,), like=q), _stream(q)))
+    return touched
+
+
 def sparse_adam(table: torch.Tensor, grad: torch.Tensor, exp_avg: torch.Tensor, exp_avg_sq: torch.Tensor,
-                step: int, lr: float = 1e-3, betas=(0.9, 0.999), eps: float = 1e-8):
+                step: int, lr: float = 1e-3, betas=(0.9, 0.999), eps: float = 1e-8,
+                touched: Optional[torch.Tensor] = None):
     """One Adam step on the rows of ``table`` whose ``grad`` row is not all zero
-    (in place; those grad rows are cleared)."""
+    (in place; those grad rows are cleared).  With ``touched`` (from
+    ``mark_touched``) only the flagged rows are visited and the flags cleared."""
     lib = load()
     N, m = _table_shape(table)
     f32 = torch.float32
-    _check(lib.lram_sparse_adam(_dev(table, "table"), _table_dtype(table), N, m,
-                                _dev(grad, "grad", f32, (N, m), like=table),
-                                _dev(exp_avg, "exp_avg", f32, (N, m), like=table),
-                                _dev(exp_avg_sq, "exp_avg_sq", f32, (N, m), like=table),
-                                int(step), float(lr), float(betas[0]), float(betas[1]), float(eps), _stream(table)))
+    args = (_dev(table, "table"), _table_dtype(table), N, m, _dev(grad, "grad", f32, (N, m), like=table),
+            _dev(exp_avg, "exp_avg", f32, (N, m), like=table), _dev(exp_avg_sq, "exp_avg_sq", f32, (N, m), like=table))
+    hyper = (int(step), float(lr), float(betas[0]), float(betas[1]), float(eps), _stream(table))
+    if touched is None:
+        _check(lib.lram_sparse_adam(*args, *hyper))
+    else:
+        _check(lib.lram_sparse_adam_touched(*args, _dev(touched, "touched", torch.uint8, (N,), like=table), *hyper))
 
 
 class SparseAdam:
@@ -497,6 +520,9 @@ class SparseAdam:
         self.exp_avg = torch.zeros(table.shape, dtype=torch.float32, device=table.device)
         self.exp_avg_sq = torch.zeros(table.shape, dtype=torch.float32, device=table.device)
 
-    def step(self, grad: torch.Tensor):
+    def step(self, grad: torch.Tensor, touched: Optional[torch.Tensor] = None):
+        """touched: flags from ``mark_touched`` for the step's lookups (the step
+        then visits only those rows)."""
         self.t += 1
-        sparse_adam(self.table, grad, self.exp_avg, self.exp_avg_sq, self.t, self.lr, self.betas, self.eps)
+        sparse_adam(self.table, grad, self.exp_avg, self.exp_avg_sq, self.t, self.lr, self.betas, self.eps,
+                    touched=touched)

@@ -749,8 +749,10 @@ int lram_access_stats(const float* hist, int64_t N, double* out, void* stream) {
   return launched();
 }
 
-int lram_sparse_adam(void* table, int dtype, int64_t N, int32_t m, float* grad, float* exp_avg, float* exp_avg_sq,
-                     int64_t step, double lr, double beta1, double beta2, double eps, void* stream) {
+// Checks of the Adam entry points and their step constants (1 - beta and the
+// bias corrections formed in fp64, rounded once).
+static int adam_args(void* table, int dtype, int64_t N, int32_t m, float* grad, float* exp_avg, float* exp_avg_sq,
+                     int64_t step, double lr, double beta1, double beta2, double eps, AdamArgs* a) {
   if (dtype != LRAM_F32 && dtype != LRAM_BF16) return LRAM_EDTYPE;
   if (m != 32 && m != 64) return LRAM_EDTYPE;
   if (N < 0 || step < 1 || !(lr >= 0.0) || !(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0) ||
@@ -759,15 +761,22 @@ int lram_sparse_adam(void* table, int dtype, int64_t N, int32_t m, float* grad, 
   if (N == 0) return LRAM_OK;
   for (const void* ptr : {(const void*)table, (const void*)grad, (const void*)exp_avg, (const void*)exp_avg_sq})
     if (!ptr || misaligned16(ptr)) return LRAM_EINVAL;
+  a->lr = (float)lr;
+  a->beta1 = (float)beta1;
+  a->beta2 = (float)beta2;
+  a->eps = (float)eps;
+  a->om1 = (float)(1.0 - beta1);
+  a->om2 = (float)(1.0 - beta2);
+  a->bc1 = (float)(1.0 - std::pow(beta1, (double)step));
+  a->bc2 = (float)(1.0 - std::pow(beta2, (double)step));
+  return LRAM_OK;
+}
+
+int lram_sparse_adam(void* table, int dtype, int64_t N, int32_t m, float* grad, float* exp_avg, float* exp_avg_sq,
+                     int64_t step, double lr, double beta1, double beta2, double eps, void* stream) {
   AdamArgs a;
-  a.lr = (float)lr;
-  a.beta1 = (float)beta1;
-  a.beta2 = (float)beta2;
-  a.eps = (float)eps;
-  a.om1 = (float)(1.0 - beta1);
-  a.om2 = (float)(1.0 - beta2);
-  a.bc1 = (float)(1.0 - std::pow(beta1, (double)step));
-  a.bc2 = (float)(1.0 - std::pow(beta2, (double)step));
+  if (int rc = adam_args(table, dtype, N, m, grad, exp_avg, exp_avg_sq, step, lr, beta1, beta2, eps, &a)) return rc;
+  if (N == 0) return LRAM_OK;
   const int64_t rows_per_block = (int64_t)WAVES * (WAVE / m);
   int64_t blocks = (N + rows_per_block - 1) / rows_per_block;
   blocks = blocks < 16384 ? blocks : 16384;
@@ -777,6 +786,36 @@ int lram_sparse_adam(void* table, int dtype, int64_t N, int32_t m, float* grad, 
   if (dtype == LRAM_F32 && m == 64) hipLaunchKernelGGL((k_sparse_adam<LRAM_F32, 64>), g, b, 0, s, table, N, grad, exp_avg, exp_avg_sq, a);
   if (dtype == LRAM_BF16 && m == 32) hipLaunchKernelGGL((k_sparse_adam<LRAM_BF16, 32>), g, b, 0, s, table, N, grad, exp_avg, exp_avg_sq, a);
   if (dtype == LRAM_BF16 && m == 64) hipLaunchKernelGGL((k_sparse_adam<LRAM_BF16, 64>), g, b, 0, s, table, N, grad, exp_avg, exp_avg_sq, a);
+  return launched();
+}
+
+int lram_mark_touched(const float* q, int64_t B, int64_t H, const int32_t K[8], uint8_t* touched, void* stream) {
+  int64_t L;
+  Params P;
+  int rc = check_common(q, B, H, K, &L, &P);
+  if (rc) return rc;
+  if (L == 0) return LRAM_OK;
+  if (!touched) return LRAM_EINVAL;
+  hipLaunchKernelGGL(k_mark_touched, dim3(grid_for(P)), dim3(THREADS), 0, (hipStream_t)stream, q, P, touched);
+  return launched();
+}
+
+int lram_sparse_adam_touched(void* table, int dtype, int64_t N, int32_t m, float* grad, float* exp_avg,
+                             float* exp_avg_sq, uint8_t* touched, int64_t step, double lr, double beta1, double beta2,
+                             double eps, void* stream) {
+  AdamArgs a;
+  if (int rc = adam_args(table, dtype, N, m, grad, exp_avg, exp_avg_sq, step, lr, beta1, beta2, eps, &a)) return rc;
+  if (N == 0) return LRAM_OK;
+  if (!touched) return LRAM_EINVAL;
+  const int64_t rows_per_block = (int64_t)WAVES * WAVE;
+  int64_t blocks = (N + rows_per_block - 1) / rows_per_block;
+  blocks = blocks < 16384 ? blocks : 16384;
+  const dim3 g((unsigned)blocks), b(THREADS);
+  hipStream_t s = (hipStream_t)stream;
+  if (dtype == LRAM_F32 && m == 32) hipLaunchKernelGGL((k_sparse_adam_touched<LRAM_F32, 32>), g, b, 0, s, table, N, grad, exp_avg, exp_avg_sq, touched, a);
+  if (dtype == LRAM_F32 && m == 64) hipLaunchKernelGGL((k_sparse_adam_touched<LRAM_F32, 64>), g, b, 0, s, table, N, grad, exp_avg, exp_avg_sq, touched, a);
+  if (dtype == LRAM_BF16 && m == 32) hipLaunchKernelGGL((k_sparse_adam_touched<LRAM_BF16, 32>), g, b, 0, s, table, N, grad, exp_avg, exp_avg_sq, touched, a);
+  if (dtype == LRAM_BF16 && m == 64) hipLaunchKernelGGL((k_sparse_adam_touched<LRAM_BF16, 64>), g, b, 0, s, table, N, grad, exp_avg, exp_avg_sq, touched, a);
   return launched();
 }
 

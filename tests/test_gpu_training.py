@@ -7,7 +7,10 @@ gives used = 1 and KL = 0.  Adam: moments per row relative <= 1e-6, the step
 (new - old value) per row relative <= 1e-4 (fp32 table entries of size 0.02
 carry 2e-9 of rounding against steps of size lr), bf16 tables within one bf16
 unit of the rounded fp64 result plus the fp32 rounding of the step; untouched
-rows bit-identical; used gradient rows cleared.
+rows bit-identical; used gradient rows cleared.  The touched-row step
+(flags from lram_mark_touched) is bit-identical to the full-scan step on
+table, moments and gradient, and leaves every flag cleared; the flags mark
+exactly the oracle's locations of the lookups.
 """
 import itertools
 
@@ -118,3 +121,32 @@ def test_training_step_roundtrip():
     moved = (table != before).any(1)
     assert torch.equal(moved, read)
     assert torch.count_nonzero(gt).item() == 0
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("m", [32, 64])
+def test_sparse_adam_touched_matches_full_scan(m, dtype):
+    K = (4, 4, 4, 4, 8, 8, 8, 8)
+    N = int(np.prod(K))
+    rng = np.random.default_rng(8)
+    q_np = (rng.random((3000, 8)) * np.asarray(K)).astype(np.float32)
+    q_np[7] = np.nan                       # no neighbours
+    q = torch.from_numpy(q_np).to(DEV)
+    touched = lram.mark_touched(q, K)
+    nb = oracle.neighbors(q_np, K)
+    ref = np.zeros(N, bool)
+    ref[nb["slot"][nb["slot"] >= 0]] = True
+    assert np.array_equal(touched.cpu().numpy() != 0, ref)
+    table = (torch.randn((N, m), device=DEV) * 0.02).to(dtype)
+    G = torch.randn((3000, m), device=DEV)
+    G[11] = 0.0                            # a lookup whose rows get no gradient from it
+    gt, _ = lram.backward(q, table.float() if dtype == torch.float32 else table, K, G, want_grad_q=False,
+                          mode="merged")
+    e1 = (torch.randn((N, m), device=DEV) * 1e-3)
+    e2 = torch.rand((N, m), device=DEV) * 1e-4
+    t2, g2, a1, a2 = table.clone(), gt.clone(), e1.clone(), e2.clone()
+    lram.sparse_adam(table, gt, e1, e2, step=5, lr=1e-3)
+    lram.sparse_adam(t2, g2, a1, a2, step=5, lr=1e-3, touched=touched)
+    torch.cuda.synchronize()
+    assert torch.equal(table, t2) and torch.equal(e1, a1) and torch.equal(e2, a2) and torch.equal(gt, g2)
+    assert torch.count_nonzero(touched).item() == 0
