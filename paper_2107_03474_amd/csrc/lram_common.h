@@ -145,6 +145,17 @@ __device__ __forceinline__ int prefix_count(uint64_t mask) {
 
 __device__ __forceinline__ uint32_t uniform(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// Keeps prefetch loads (lines fetched into L2 ahead of atomics on them) alive:
+// their values meet here only, in a store that never happens (never is a
+// condition false whenever the kernel runs correctly).
+template <int NP>
+__device__ __forceinline__ void sink_prefetch(const uint32_t (&v)[NP], bool never, float* __restrict__ dst) {
+  uint32_t x = 0;
+#pragma unroll
+  for (int k = 0; k < NP; ++k) x ^= v[k];
+  if (never && x == 0x7FC00001u) dst[0] = 0.0f;
+}
+
 // Orders LDS traffic between lanes of one wave: the wave's LDS operations
 // execute in issue order, so a compiler barrier is enough.
 __device__ __forceinline__ void wave_lds_sync() {

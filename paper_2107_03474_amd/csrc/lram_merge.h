@@ -351,6 +351,22 @@ __global__ void __launch_bounds__(THREADS, (merge_waves_per_simd<DT, M, KS>())) 
 #pragma unroll
   for (int k = 0; k < MERGE_HPT / 2; ++k) MW.cnt[t * (MERGE_HPT / 2) + k] = first[2 * k] | (first[2 * k + 1] << 16);
   __syncthreads();
+  // rows of 32 columns (one 128-byte line): fetch the line of every distinct
+  // location's gradient row into L2 now, so that the atomics below find it
+  // there (the values are not used: loads that nothing waits for until the
+  // kernel's end).  Rows of 64 columns measured no gain from it.
+  constexpr bool PREFETCH = M == 32;
+  uint32_t pfv[MERGE_PPT];
+#pragma unroll
+  for (int k = 0; k < MERGE_PPT; ++k) pfv[k] = 0u;
+  if constexpr (PREFETCH) {
+    const uint32_t ng = MW.ngroups;
+#pragma unroll
+    for (int k = 0; k < MERGE_PPT; ++k) {
+      const uint32_t gi = t + k * THREADS;
+      if (gi < ng) pfv[k] = reinterpret_cast<const uint32_t*>(gtab)[(size_t)tag[gi] * M];
+    }
+  }
   // pairs into group order: weights in the upper half of the tag array
   float* pw = reinterpret_cast<float*>(tag + MERGE_P);
   uint8_t* pt = MW.pt;
@@ -396,6 +412,7 @@ __global__ void __launch_bounds__(THREADS, (merge_waves_per_simd<DT, M, KS>())) 
     for (int u = 0; u < U; ++u)
       if (loc[u] >= 0) unsafeAtomicAdd(gtab + (size_t)loc[u] * M + col, acc[u]);
   }
+  if constexpr (PREFETCH) sink_prefetch(pfv, ngroups > (uint32_t)MERGE_P, gtab);
 }
 
 }  // namespace
