@@ -319,12 +319,23 @@ int build_order(const float* q, const Params& P, const OrderWs& o, hipStream_t s
     std::swap(r.ka, r.kb);
     std::swap(r.va, r.vb);
   }
-  const dim3 kgrid((unsigned)((P.L + THREADS - 1) / THREADS));
-  hipLaunchKernelGGL(k_cell_key<TH>, kgrid, dim3(THREADS), 0, s, q, P, r.ka);
+  // clear the sort's header (digit counts, failure word, gate partials); the
+  // key kernel counts the digits and clears the look-back states
+  const int passes = radix_passes(P.N);
+  const bool small = r.n < SORT_SMALL_STATES;
+  const int64_t state_words = (int64_t)passes * r.states * RADIX * (small ? 1 : 2);
+  hipLaunchKernelGGL(k_zero_words, dim3((unsigned)((SORT_HDR_WORDS + THREADS - 1) / THREADS)), dim3(THREADS), 0, s,
+                     r.hdr, (int64_t)SORT_HDR_WORDS);
+  const int64_t kb = (P.L + THREADS - 1) / THREADS;
+  hipLaunchKernelGGL(k_cell_key<TH>, dim3((unsigned)(kb < 1024 ? kb : 1024)), dim3(THREADS), 0, s, q, P, r.ka, passes,
+                     r.hdr, reinterpret_cast<uint32_t*>(r.state), state_words);
   if (int rc = launched()) return rc;
-  if (int rc = radix_sort<uint32_t, true>(r, P.N, s)) return rc;
-  const int64_t cb = (P.L + THREADS - 1) / THREADS;
-  hipLaunchKernelGGL(k_count_shared, dim3((unsigned)(cb < 1024 ? cb : 1024)), dim3(THREADS), 0, s,
+  if (int rc = small ? radix_passes_run<uint32_t, true, uint32_t>(r, passes, s)
+                     : radix_passes_run<uint32_t, true, uint64_t>(r, passes, s))
+    return rc;
+  // COUNT_UNROLL positions per thread: one round of loads
+  const int64_t cb = (P.L + THREADS * COUNT_UNROLL - 1) / (THREADS * COUNT_UNROLL);
+  hipLaunchKernelGGL(k_count_shared, dim3((unsigned)(cb < (1 << 20) ? cb : (1 << 20))), dim3(THREADS), 0, s,
                      (const uint32_t*)o.sort.ka, P.L, r.hdr + SORT_COUNT);
   hipLaunchKernelGGL(k_count_finalize, dim3(1), dim3(WAVE), 0, s, (const uint32_t*)(r.hdr + SORT_COUNT),
                      (const uint32_t*)(r.hdr + SORT_FAIL), o.shared);

@@ -15,34 +15,71 @@ namespace {
 // than 32, see merge_t) is reduced in LDS to one fp32 atomic row per distinct
 // location of the batch.
 
-// key[l] = location of the closest point of Lambda to q_l (N for a non-finite
-// query).
+// Location of the closest point of Lambda to the query qq (N for a
+// non-finite query).
+__device__ __forceinline__ uint32_t cell_location(const float (&qq)[8], const Params P) {
+  float x[8];
+  int c[8];
+  if (!closest_point(qq, true, P, x, c)) return P.N;
+  const int eps = c[0] & 1;
+  uint32_t acc = eps ? P.N : 0u;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    // |x_i| < 2 K_i and |x_i - c_i| <= 1 put y within [-K_i - 1, K_i]: two
+    // periods up or one down bring it into [0, K_i) (K_i = 2 included)
+    int y = (c[i] - eps) >> 1;
+    y += y < 0 ? P.K[i] : 0;
+    y += y < 0 ? P.K[i] : 0;
+    y -= y >= P.K[i] ? P.K[i] : 0;
+    acc += (uint32_t)y * P.S[i];
+  }
+  return acc >> 1;
+}
+
+// key[l] = cell_location of lookup l, and the digit counts of the keys for
+// the first `passes` passes of the radix sort that orders them (as
+// k_digit_hist: each workgroup counts one contiguous chunk of lookups in
+// per-wave LDS counters and adds its nonzero bins to copy blockIdx %
+// SORT_HIST_COPIES of ghist, cleared).  The workgroups also clear the sort's
+// look-back states, clear[0, nclear), which no pass reads before this kernel
+// ends.  Each lookup's input is loaded one lookup ahead.
 template <bool TH>
 __global__ void __launch_bounds__(THREADS) k_cell_key(const float* __restrict__ q, Params P,
-                                                      uint32_t* __restrict__ key) {
-  const int64_t l = (int64_t)blockIdx.x * THREADS + threadIdx.x;
-  if (l >= P.L) return;
-  float x[8], qq[8], scale;
-  int c[8];
-  load_query<TH>(q + l * in_stride<TH>(), P, qq, scale);
-  const bool valid = closest_point(qq, true, P, x, c);
-  uint32_t loc = P.N;
-  if (valid) {
-    const int eps = c[0] & 1;
-    uint32_t acc = eps ? P.N : 0u;
+                                                      uint32_t* __restrict__ key, int passes,
+                                                      uint32_t* __restrict__ ghist, uint32_t* __restrict__ clear,
+                                                      int64_t nclear) {
+  __shared__ uint32_t h[WAVES][SORT_PASSES_MAX][RADIX];
+  const int t = threadIdx.x, w = t / WAVE;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      // |x_i| < 2 K_i and |x_i - c_i| <= 1 put y within [-K_i - 1, K_i]: two
-      // periods up or one down bring it into [0, K_i) (K_i = 2 included)
-      int y = (c[i] - eps) >> 1;
-      y += y < 0 ? P.K[i] : 0;
-      y += y < 0 ? P.K[i] : 0;
-      y -= y >= P.K[i] ? P.K[i] : 0;
-      acc += (uint32_t)y * P.S[i];
-    }
-    loc = acc >> 1;
+  for (int k = 0; k < WAVES; ++k)
+#pragma unroll
+    for (int p = 0; p < SORT_PASSES_MAX; ++p) h[k][p][t] = 0;
+  for (int64_t i = (int64_t)blockIdx.x * THREADS + t; i < nclear; i += (int64_t)gridDim.x * THREADS) clear[i] = 0u;
+  __syncthreads();
+  const int64_t chunk = (P.L + gridDim.x - 1) / gridDim.x;
+  const int64_t b = (int64_t)blockIdx.x * chunk, e = min<int64_t>(P.L, b + chunk);
+  float4 v[in_vec4<TH>()];
+  if (b + t < e) load_input<TH>(q + (b + t) * in_stride<TH>(), v);
+  for (int64_t l = b + t; l < e; l += THREADS) {
+    float4 cur[in_vec4<TH>()];
+#pragma unroll
+    for (int k = 0; k < in_vec4<TH>(); ++k) cur[k] = v[k];
+    if (l + THREADS < e) load_input<TH>(q + (l + THREADS) * in_stride<TH>(), v);
+    float qq[8], scale;
+    query_from<TH>(cur, P, qq, scale);
+    const uint32_t loc = cell_location(qq, P);
+    key[l] = loc;
+#pragma unroll
+    for (int p = 0; p < SORT_PASSES_MAX; ++p)
+      if (p < passes) atomicAdd(&h[w][p][(loc >> (p * RADIX_BITS)) & (RADIX - 1)], 1u);
   }
-  key[l] = loc;
+  __syncthreads();
+  uint32_t* g = ghist + (blockIdx.x % SORT_HIST_COPIES) * (SORT_PASSES_MAX * RADIX);
+#pragma unroll
+  for (int p = 0; p < SORT_PASSES_MAX; ++p) {
+    const uint32_t c = h[0][p][t] + h[1][p][t] + h[2][p][t] + h[3][p][t];
+    if (p < passes && c) atomicAdd(&g[p * RADIX + t], c);
+  }
 }
 
 // Activation layer coordinates: q[l] (8 fp32) and scale s[l] as the lookups see them.
@@ -58,15 +95,27 @@ __global__ void __launch_bounds__(THREADS) k_theta_coords(const float* __restric
 }
 
 // Number of positions whose sorted key equals a neighbour's, in COUNT_COPIES
-// partial counters (workgroup b adds into copy b % COUNT_COPIES, cleared, so
-// that few atomics meet on one address); k_count_finalize adds them up.
+// partial counters COUNT_STRIDE words apart (workgroup b adds into copy b %
+// COUNT_COPIES, cleared, so that few atomics meet on one line);
+// k_count_finalize adds them up.
+constexpr int COUNT_UNROLL = 4;  // positions per thread whose loads are issued together
 __global__ void __launch_bounds__(THREADS) k_count_shared(const uint32_t* __restrict__ keys, int64_t L,
                                                           uint32_t* __restrict__ copies) {
   __shared__ uint32_t wsum[WAVES];
+  constexpr int U = COUNT_UNROLL;
   uint32_t c = 0;
-  for (int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x; i < L; i += (int64_t)gridDim.x * THREADS) {
-    const uint32_t k = keys[i];
-    c += ((i > 0 && keys[i - 1] == k) || (i + 1 < L && keys[i + 1] == k)) ? 1u : 0u;
+  const int64_t stride = (int64_t)gridDim.x * THREADS;
+  for (int64_t i0 = (int64_t)blockIdx.x * THREADS + threadIdx.x; i0 < L; i0 += U * stride) {
+    uint32_t kp[U], kc[U], kn[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = i0 + u * stride;
+      kc[u] = i < L ? keys[i] : 0u;
+      kp[u] = i < L && i > 0 ? keys[i - 1] : ~kc[u];
+      kn[u] = i + 1 < L ? keys[i + 1] : ~kc[u];
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) c += (i0 + u * stride < L && (kp[u] == kc[u] || kn[u] == kc[u])) ? 1u : 0u;
   }
 #pragma unroll
   for (int mask = 1; mask < WAVE; mask <<= 1) c += __shfl_xor(c, mask);
@@ -74,7 +123,7 @@ __global__ void __launch_bounds__(THREADS) k_count_shared(const uint32_t* __rest
   __syncthreads();
   if (threadIdx.x == 0) {
     const uint32_t t = wsum[0] + wsum[1] + wsum[2] + wsum[3];
-    if (t) atomicAdd(copies + blockIdx.x % COUNT_COPIES, t);
+    if (t) atomicAdd(copies + (blockIdx.x % COUNT_COPIES) * COUNT_STRIDE, t);
   }
 }
 
@@ -83,7 +132,7 @@ __global__ void __launch_bounds__(THREADS) k_count_shared(const uint32_t* __rest
 __global__ void k_count_finalize(const uint32_t* __restrict__ copies, const uint32_t* __restrict__ sort_fail,
                                  uint32_t* __restrict__ count) {
   uint32_t s = 0;
-  for (int i = threadIdx.x; i < COUNT_COPIES; i += WAVE) s += copies[i];
+  for (int i = threadIdx.x; i < COUNT_COPIES; i += WAVE) s += copies[i * COUNT_STRIDE];
 #pragma unroll
   for (int mask = 1; mask < WAVE; mask <<= 1) s += __shfl_xor(s, mask);
   if (threadIdx.x == 0) {

@@ -34,26 +34,28 @@ __device__ __forceinline__ void d8_round(const float (&y)[8], int (&r)[8]) {
   }
 }
 
-// The query of one lookup and its output scale.  TH = false: q itself
-// (8 floats), scale 1.  TH = true, the activation layer of Sec. 2.3: z_i =
-// in[2i] + i in[2i+1], q_i = (K_i / 2 pi) arg z_i formed in fp64 and rounded
-// once to fp32, scale (sum_i 1/|z_i|)^-1 (0 when some z_i = 0); a non-finite
-// input gives a NaN query (empty neighbour list) and scale 0.
+// Input float4s per lookup: q (8 floats) or z (16, the activation layer).
 template <bool TH>
-__device__ __forceinline__ void load_query(const float* __restrict__ in, const Params P, float (&qq)[8],
+constexpr int in_vec4() { return TH ? 4 : 2; }
+
+// The query of one lookup and its output scale, from the lookup's input
+// vectors v.  TH = false: q itself (8 floats), scale 1.  TH = true, the
+// activation layer of Sec. 2.3: z_i = in[2i] + i in[2i+1], q_i = (K_i / 2 pi)
+// arg z_i formed in fp64 and rounded once to fp32, scale (sum_i 1/|z_i|)^-1 (0
+// when some z_i = 0); a non-finite input gives a NaN query (empty neighbour
+// list) and scale 0.
+template <bool TH>
+__device__ __forceinline__ void query_from(const float4 (&v)[in_vec4<TH>()], const Params P, float (&qq)[8],
                                            float& scale) {
   if constexpr (!TH) {
-    const float4 a = reinterpret_cast<const float4*>(in)[0];
-    const float4 b = reinterpret_cast<const float4*>(in)[1];
-    qq[0] = a.x; qq[1] = a.y; qq[2] = a.z; qq[3] = a.w;
-    qq[4] = b.x; qq[5] = b.y; qq[6] = b.z; qq[7] = b.w;
+    qq[0] = v[0].x; qq[1] = v[0].y; qq[2] = v[0].z; qq[3] = v[0].w;
+    qq[4] = v[1].x; qq[5] = v[1].y; qq[6] = v[1].z; qq[7] = v[1].w;
     scale = 1.0f;
   } else {
     float z[16];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      const float4 v = reinterpret_cast<const float4*>(in)[k];
-      z[4 * k] = v.x; z[4 * k + 1] = v.y; z[4 * k + 2] = v.z; z[4 * k + 3] = v.w;
+      z[4 * k] = v[k].x; z[4 * k + 1] = v[k].y; z[4 * k + 2] = v[k].z; z[4 * k + 3] = v[k].w;
     }
     bool finite = true;
     double inv = 0.0;
@@ -67,6 +69,20 @@ __device__ __forceinline__ void load_query(const float* __restrict__ in, const P
     if (!finite) qq[0] = __builtin_nanf("");
     scale = finite ? (float)(1.0 / inv) : 0.0f;
   }
+}
+
+template <bool TH>
+__device__ __forceinline__ void load_input(const float* __restrict__ in, float4 (&v)[in_vec4<TH>()]) {
+#pragma unroll
+  for (int k = 0; k < in_vec4<TH>(); ++k) v[k] = reinterpret_cast<const float4*>(in)[k];
+}
+
+template <bool TH>
+__device__ __forceinline__ void load_query(const float* __restrict__ in, const Params P, float (&qq)[8],
+                                           float& scale) {
+  float4 v[in_vec4<TH>()];
+  load_input<TH>(in, v);
+  query_from<TH>(v, P, qq, scale);
 }
 
 // Wrapped Lambda-scale query x and the closest point c of Lambda (either coset);

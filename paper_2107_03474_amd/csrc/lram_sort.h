@@ -55,12 +55,15 @@ constexpr int LOOKBACK_GROUP = 32;
 // SORT_HIST_COPIES copies [copy][pass][RADIX] (workgroup b adds into copy b %
 // SORT_HIST_COPIES: atomics on one address serialise in memory, about 35 ns
 // each), the failure word, the lookup order's gate-count partials
-// [COUNT_COPIES]; then the tile states.
+// [COUNT_COPIES], one to a 128-byte line (atomics on one line serialise
+// too); then the tile states.
 constexpr int SORT_HIST_COPIES = 16;
 constexpr int SORT_FAIL = SORT_HIST_COPIES * SORT_PASSES_MAX * RADIX;
 constexpr int SORT_COUNT = SORT_FAIL + 64;
 constexpr int COUNT_COPIES = 64;
-constexpr int SORT_HDR_WORDS = SORT_COUNT + COUNT_COPIES;
+constexpr int COUNT_STRIDE = 32;  // words between gate-count partials
+constexpr int SORT_HDR_WORDS = SORT_COUNT + COUNT_COPIES * COUNT_STRIDE;
+static_assert((SORT_COUNT * 4) % 128 == 0, "gate-count partials start on a line");
 
 __global__ void __launch_bounds__(THREADS) k_zero_words(uint32_t* __restrict__ p, int64_t n) {
   for (int64_t i = (int64_t)blockIdx.x * THREADS + threadIdx.x; i < n; i += (int64_t)gridDim.x * THREADS) p[i] = 0u;
@@ -194,13 +197,10 @@ __global__ void __launch_bounds__(THREADS, 4) k_onesweep(const uint32_t* __restr
   const int64_t base = tile * SORT_TILE;
   const int cnt = (int)min<int64_t>(SORT_TILE, n - base);
   uint32_t key[SORT_ROUNDS];
-  V val[IDENT ? 1 : SORT_ROUNDS];  // IDENT: the payload is formed when it is staged
 #pragma unroll
   for (int r = 0; r < SORT_ROUNDS; ++r) {
     const int j = w * SORT_WAVE_ELEMS + r * WAVE + lane;
-    const bool valid = j < cnt;
-    key[r] = valid ? kin[base + j] : 0u;
-    if constexpr (!IDENT) val[r] = valid ? vin[base + j] : V{};
+    key[r] = j < cnt ? kin[base + j] : 0u;
   }
   // rank inside the wave: earlier rounds' count of the digit + lanes below
   // with the same digit in this round
@@ -237,6 +237,16 @@ __global__ void __launch_bounds__(THREADS, 4) k_onesweep(const uint32_t* __restr
   S* tstate = state;                    // [tiles][RADIX]: AGGREGATE | count
   S* gstate = state + tiles * RADIX;    // [groups][RADIX]
   __hip_atomic_store(tstate + tile * RADIX + t, C::AGGREGATE | (S)c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  // the payloads are loaded now, so that the ranking above had the memory
+  // system to the keys alone and the loads overlap the look-back
+  V val[IDENT ? 1 : SORT_ROUNDS];  // IDENT: the payload is formed when it is staged
+  if constexpr (!IDENT) {
+#pragma unroll
+    for (int r = 0; r < SORT_ROUNDS; ++r) {
+      const int j = w * SORT_WAVE_ELEMS + r * WAVE + lane;
+      val[r] = j < cnt ? vin[base + j] : V{};
+    }
+  }
   dstart[t] = block_exclusive_scan(c, part[1]);
   __syncthreads();
   // each element's position in the tile's digit order (two 12-bit positions
