@@ -19,7 +19,8 @@ Output (``e8_candidates.inc``):
     ascending order of that distance, and E8_FAST / E8_FAST_BOUND: the first
     E8_FAST of them and the exact distance^2 from F of every later one, at
     least E8_FAST_BOUND (a query in F whose k-th closest point among the
-    first E8_FAST lies below that bound takes its closest k from them);
+    first E8_FAST lies below that bound takes its closest k from them), and
+    the same for the first E8_FAST2 (E8_FAST2_BOUND), a smaller first tier;
   * the BOUNDARY list -- dist(p, F)^2 == 8 exactly.  These never lie in the open
     support of a query inside F, but a query whose reduction lands a rounding
     error outside F, or whose fp32 distance rounds below 8, can see them; the
@@ -39,6 +40,7 @@ OUT = os.path.join(HERE, "e8_candidates.inc")
 
 
 FAST = 192  # three candidates per lane of a 64-lane wave
+FAST2 = 128  # two per lane: the first tier of the fast set
 
 
 def lattice_points(max_norm: int) -> np.ndarray:
@@ -146,6 +148,7 @@ def main(write: bool = True) -> dict:
     strict_d2 = [e[0] for e in strict]
     strict = [e[1] for e in strict]
     fast_bound = strict_d2[FAST] if FAST < len(strict) else Fraction(8)
+    fast2_bound = strict_d2[FAST2]
     boundary = sorted(boundary, key=lambda v: (int((v * v).sum()), tuple(-v)))
     gap = min(above) - 8.0
     norms = {}
@@ -153,7 +156,8 @@ def main(write: bool = True) -> dict:
         norms[int((v * v).sum())] = norms.get(int((v * v).sum()), 0) + 1
     allpts = np.array(strict + boundary)
     info = dict(strict=np.array(strict), boundary=np.array(boundary), gap=gap, norms=norms,
-                cmin=int(allpts.min()), cmax=int(allpts.max()), strict_d2=strict_d2, fast_bound=fast_bound)
+                cmin=int(allpts.min()), cmax=int(allpts.max()), strict_d2=strict_d2, fast_bound=fast_bound,
+                fast2_bound=fast2_bound)
     if write:
         with open(OUT, "w") as f:
             f.write("// Generated by gen_e8_candidates.py -- do not edit.\n")
@@ -165,6 +169,8 @@ def main(write: bool = True) -> dict:
             f.write("#define E8_CAND_MIN %d\n#define E8_CAND_MAX %d\n" % (info["cmin"], info["cmax"]))
             f.write("// Strict points FAST.. lie at distance^2 >= %s from F.\n" % fast_bound)
             f.write("#define E8_FAST %d\n#define E8_FAST_BOUND %.9gf\n" % (FAST, float(fast_bound)))
+            f.write("// Strict points FAST2.. lie at distance^2 >= %s from F.\n" % fast2_bound)
+            f.write("#define E8_FAST2 %d\n#define E8_FAST2_BOUND %.9gf\n" % (FAST2, float(fast2_bound)))
             for name, lst in (("E8_STRICT_INIT", strict), ("E8_BOUNDARY_INIT", boundary)):
                 f.write("#define %s { \\\n" % name)
                 for v in lst:

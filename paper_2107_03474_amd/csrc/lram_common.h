@@ -15,7 +15,9 @@ constexpr int NS_STRICT = (E8_NSTRICT + WAVE - 1) / WAVE;      // 4 candidate sl
 constexpr int NS_BOUND = (E8_NBOUNDARY + WAVE - 1) / WAVE;     // 3
 constexpr int NS_ALL = NS_STRICT + NS_BOUND;
 constexpr int NS_FAST = E8_FAST / WAVE;                          // 3: the fast set's slots per lane
+constexpr int NS_FAST2 = E8_FAST2 / WAVE;                        // 2: its first tier
 static_assert(E8_FAST % WAVE == 0 && NS_FAST < NS_STRICT, "the fast candidate set fills whole slots");
+static_assert(E8_FAST2 % WAVE == 0 && NS_FAST2 < NS_FAST, "the first tier fills whole slots");
 constexpr int CMIN = E8_CAND_MIN;
 constexpr int NV = E8_CAND_MAX - E8_CAND_MIN + 1;
 static_assert(NV == 8, "each per-query table row holds the 8 possible candidate coordinate values");
@@ -45,8 +47,10 @@ constexpr uint32_t KEY_SUSPECT = 0x40FFF7CFu;  // 7.999f
 // A query whose k-th closest candidate among the first E8_FAST lies below
 // KEY_FAST takes its closest k from them: every later candidate lies at
 // distance^2 >= E8_FAST_BOUND from F, and the reduction puts a query within
-// about 1e-5 (in distance^2) of F, far inside the 2^-7 margin.
+// about 1e-5 (in distance^2) of F, far inside the 2^-7 margin.  The same
+// holds for the first E8_FAST2 candidates and KEY_FAST2, tried first.
 constexpr uint32_t KEY_FAST = __builtin_bit_cast(uint32_t, E8_FAST_BOUND - 0.0078125f);
+constexpr uint32_t KEY_FAST2 = __builtin_bit_cast(uint32_t, E8_FAST2_BOUND - 0.0078125f);
 
 __constant__ signed char c_strict[E8_NSTRICT][8] = E8_STRICT_INIT;
 __constant__ signed char c_boundary[E8_NBOUNDARY][8] = E8_BOUNDARY_INIT;

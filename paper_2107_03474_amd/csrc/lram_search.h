@@ -519,16 +519,30 @@ struct Search {
       int need = 0;
       bool suspect = true;
       bool fast = false;
-      // lists of up to 32: scan the E8_FAST candidates nearest to F first;
-      // when the ks-th closest of them is below KEY_FAST none of the others
-      // can be among the closest ks (nearly every query)
+      // lists of up to 32: scan the E8_FAST2 candidates nearest to F first,
+      // then the E8_FAST nearest; when the ks-th closest of a set is below
+      // its bound none of the others can be among the closest ks (about 9 in
+      // 10 queries take the first set, nearly every other the second)
       uint32_t key3[NS_FAST];
       if constexpr (KS <= NB) {
+        uint32_t key2[NS_FAST2];
 #pragma unroll
-        for (int k = 0; k < NS_FAST; ++k) key3[k] = __float_as_uint(cand_d2(S.qt, lo[k], hi[k], sel));
-        count = threshold_k_hist<NS_FAST>(key3, W.hist, lane, KS, thr, tie_key, need, suspect);
-        fast = count == KS && !suspect && (tie_key != KEY_INF ? tie_key < KEY_FAST : thr <= KEY_FAST);
-        if (fast) emit<NS_FAST>(key3, thr, tie_key, need, sel, F, buf);
+        for (int k = 0; k < NS_FAST2; ++k) key2[k] = key3[k] = __float_as_uint(cand_d2(S.qt, lo[k], hi[k], sel));
+        count = threshold_k_hist<NS_FAST2>(key2, W.hist, lane, KS, thr, tie_key, need, suspect);
+        fast = count == KS && !suspect && (tie_key != KEY_INF ? tie_key < KEY_FAST2 : thr <= KEY_FAST2);
+        if (fast) {
+          emit<NS_FAST2>(key2, thr, tie_key, need, sel, F, buf);
+        } else {
+#pragma unroll
+          for (int k = NS_FAST2; k < NS_FAST; ++k) key3[k] = __float_as_uint(cand_d2(S.qt, lo[k], hi[k], sel));
+          thr = KEY_8;
+          tie_key = KEY_INF;
+          need = 0;
+          suspect = true;
+          count = threshold_k_hist<NS_FAST>(key3, W.hist, lane, KS, thr, tie_key, need, suspect);
+          fast = count == KS && !suspect && (tie_key != KEY_INF ? tie_key < KEY_FAST : thr <= KEY_FAST);
+          if (fast) emit<NS_FAST>(key3, thr, tie_key, need, sel, F, buf);
+        }
       }
       if (!fast) {
         uint32_t key[NS_STRICT];

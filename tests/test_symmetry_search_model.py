@@ -10,6 +10,7 @@ exactly; it validates the candidate table and the reduction on the CPU.
 """
 import os
 import re
+from fractions import Fraction
 
 import numpy as np
 import pytest
@@ -34,15 +35,17 @@ def _read_lists():
 STRICT, BOUNDARY = _read_lists()
 
 
-def _read_fast():
+def _read_fast(suffix=""):
     txt = open(INC).read()
-    n = int(re.search(r"#define E8_FAST (\d+)", txt).group(1))
-    bound = float(re.search(r"#define E8_FAST_BOUND ([\d.]+)f", txt).group(1))
+    n = int(re.search(r"#define E8_FAST%s (\d+)" % suffix, txt).group(1))
+    bound = float(re.search(r"#define E8_FAST%s_BOUND ([\d.]+)f" % suffix, txt).group(1))
     return n, bound
 
 
 FAST, FAST_BOUND = _read_fast()
 FAST_LIMIT = np.float32(FAST_BOUND - 2.0 ** -7)   # the kernels' margin
+FAST2, FAST2_BOUND = _read_fast("2")              # the first tier
+FAST2_LIMIT = np.float32(FAST2_BOUND - 2.0 ** -7)
 
 
 def _d8_round(y):
@@ -88,8 +91,10 @@ def _recipe(x, k):
 
 
 def model_neighbors(q, K, fast=False):
-    """fast: first the FAST candidates nearest to F; their closest 32 stand
-    when the 32nd is below the bound every later candidate respects."""
+    """fast: first the FAST2 candidates nearest to F, then the FAST nearest;
+    a set's closest 32 stand when the 32nd is below the bound every later
+    candidate respects.  Returns also the number of lookups that needed the
+    full scan and the number served by the first tier."""
     K = np.asarray(K)
     x = np.fmod(np.float32(2) * q, (2 * K).astype(np.float32)).astype(np.float32)
     c, r, s = _reduce(x)
@@ -103,12 +108,16 @@ def model_neighbors(q, K, fast=False):
     out_slots = np.full((q.shape[0], 32), -1, np.int64)
     suspects = 0
     fallbacks = 0
+    first_tier = 0
     for l in range(q.shape[0]):
         d, k = dS[l], kS[l]
         if fast:
-            dF = np.sort(d[:FAST])
-            if dF.size >= 32 and dF[31] < FAST_LIMIT:
-                d, k = d[:FAST], k[:FAST]
+            for n_set, limit in ((FAST2, FAST2_LIMIT), (FAST, FAST_LIMIT)):
+                dF = np.sort(d[:n_set])
+                if dF.size >= 32 and dF[31] < limit:
+                    first_tier += n_set == FAST2
+                    d, k = d[:n_set], k[:n_set]
+                    break
             else:
                 fallbacks += 1
         keep = d < np.float32(8)
@@ -128,7 +137,7 @@ def model_neighbors(q, K, fast=False):
         order = np.lexsort(tuple(k[:, i] for i in range(7, -1, -1)) + (slot, bits))[:32]
         out_slots[l, :order.size] = slot[order]
     if fast:
-        return out_slots, suspects, fallbacks
+        return out_slots, suspects, fallbacks, first_tier
     return out_slots, suspects
 
 
@@ -183,7 +192,8 @@ def test_model_special_points():
 def test_fast_set_bound_is_exact():
     """Every strict candidate after the first E8_FAST lies at least
     E8_FAST_BOUND from F (exact distances from the generator's quadratic
-    programs), and the first E8_FAST are the nearest to F."""
+    programs), and the first E8_FAST are the nearest to F; likewise the first
+    E8_FAST2 and E8_FAST2_BOUND (48/7)."""
     import importlib.util
     spec = importlib.util.spec_from_file_location(
         "gen", os.path.join(ROOT, "paper_2107_03474_amd", "csrc", "gen_e8_candidates.py"))
@@ -191,8 +201,10 @@ def test_fast_set_bound_is_exact():
     spec.loader.exec_module(gen)
     d2, sets = gen.project_all(STRICT)
     exact = [gen.exact_dist2(STRICT[i], sets[i]) for i in range(STRICT.shape[0])]
-    assert FAST == 192 and FAST % 64 == 0
+    assert FAST == 192 and FAST % 64 == 0 and FAST2 == 128 and FAST2 % 64 == 0
     assert min(exact[FAST:]) >= FAST_BOUND and max(exact[:FAST]) <= min(exact[FAST:])
+    assert min(exact[FAST2:]) == Fraction(48, 7) and max(exact[:FAST2]) <= min(exact[FAST2:])
+    assert abs(FAST2_BOUND - 48 / 7) < 1e-7
     assert all(exact[i] <= exact[i + 1] for i in range(len(exact) - 1))
 
 
@@ -209,7 +221,8 @@ def test_fast_set_model_matches_oracle(K):
     q[500:600] = np.floor(q[500:600])                       # lattice points and deep holes
     q[600:700] = np.floor(q[600:700]) + 1e-6 * rng.standard_normal((100, 8))
     q = q.astype(np.float32)
-    got, _, fallbacks = model_neighbors(q, K, fast=True)
+    got, _, fallbacks, first_tier = model_neighbors(q, K, fast=True)
     nb = oracle.neighbors(q, K)
     np.testing.assert_array_equal(got, nb["slot"])
     assert fallbacks < n // 4
+    assert first_tier > n // 2
