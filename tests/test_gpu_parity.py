@@ -105,6 +105,56 @@ def test_neighbors_dyadic_grid():
     check_neighbors(q, K)
 
 
+def _tier_band_queries(K, seed):
+    """Queries for each path of the search's fast candidate set, chosen by the
+    oracle's fp32 distance of the 32nd neighbour d: below the first tier's
+    limit 48/7 - 2^-7 (band a), within 1e-3 of it, between it and the second
+    tier's limit 15/2 - 2^-7 (band b), within 2e-3 of that, and above it or
+    with fewer than 32 points in the support (the full scan).  Noise of
+    0.05-0.1 around the deep holes spreads d over all of them."""
+    rng = np.random.default_rng(seed)
+    Kf = np.asarray(K, np.float64)
+    holes = np.array([[1, 0, 0, 0, 0, 0, 0, 0.0], [0.5] * 8, [0.5] * 7 + [-0.5]])
+    parts = [np.mod(h + 1.0 + sc * rng.standard_normal((1500, 8)), Kf) for h in holes for sc in (0.05, 0.1)]
+    parts.append(rng.random((3000, 8)) * Kf)
+    q = np.concatenate(parts).astype(np.float32)
+    nb = oracle.neighbors(q, K)
+    d = np.where(nb["count"] >= 32, nb["d2"][:, 31], np.inf)
+    lim2 = np.float32(np.float32(48 / 7) - np.float32(2.0 ** -7))
+    lim1 = np.float32(7.5 - 2.0 ** -7)
+    bands = {"a": d < lim2 - 1e-3, "a|b": np.abs(d - lim2) < 1e-3, "b": (d >= lim2 + 1e-3) & (d < lim1 - 2e-3),
+             "b|full": np.abs(d - lim1) < 2e-3, "full": d >= lim1 + 2e-3}
+    pick = []
+    for name, m in bands.items():
+        idx = np.nonzero(m)[0]
+        assert idx.size >= (5 if "|" in name else 100), (name, idx.size)
+        pick.append(idx[:300])
+    return q[np.concatenate(pick)]
+
+
+@pytest.mark.parametrize("K", [(4,) * 8, (14,) * 8])
+def test_neighbors_each_fast_tier(K):
+    """Lists of queries taken by each tier of the fast candidate set, by the
+    full scan, and at the tiers' edges: bit-exact locations, distances and
+    weights; for the 4^8 torus also the forward in its full launch
+    configuration (64 lookups per wave, lists double-buffered), with the
+    queries spread over 262,144 lookups."""
+    _say("neighbors per fast tier K=%s" % (K,))
+    q_np = _tier_band_queries(K, 17)
+    nb = check_neighbors(q_np, K)
+    if K != (4,) * 8:
+        return
+    reps = -(-262144 // q_np.shape[0])
+    perm = np.random.default_rng(4).permutation(reps * q_np.shape[0])
+    idx = np.tile(np.arange(q_np.shape[0]), reps)[perm]
+    table = _small_table(K, 32, torch.float32)
+    out = lram.forward(torch.from_numpy(q_np[idx]).to(DEV), table, K)
+    torch.cuda.synchronize()
+    ref = oracle.forward(nb, oracle.gather_rows(table.cpu().numpy(), nb["slot"]))
+    err = _rel_rows(out.cpu().numpy(), ref[idx])
+    assert err.max() <= 1e-5, err.max()
+
+
 def test_neighbors_nonfinite_and_ragged():
     _say("neighbors nonfinite/ragged")
     K = (4,) * 8
