@@ -90,11 +90,12 @@ def _recipe(x, k):
     return d
 
 
-def model_neighbors(q, K, fast=False):
+def model_neighbors(q, K, fast=False, tiers=None):
     """fast: first the FAST2 candidates nearest to F, then the FAST nearest;
     a set's closest 32 stand when the 32nd is below the bound every later
     candidate respects.  Returns also the number of lookups that needed the
-    full scan and the number served by the first tier."""
+    full scan and the number served by the first tier.  tiers: (count,
+    limit) pairs in place of the table's (a test plants a wrong bound there)."""
     K = np.asarray(K)
     x = np.fmod(np.float32(2) * q, (2 * K).astype(np.float32)).astype(np.float32)
     c, r, s = _reduce(x)
@@ -112,7 +113,7 @@ def model_neighbors(q, K, fast=False):
     for l in range(q.shape[0]):
         d, k = dS[l], kS[l]
         if fast:
-            for n_set, limit in ((FAST2, FAST2_LIMIT), (FAST, FAST_LIMIT)):
+            for n_set, limit in (tiers or ((FAST2, FAST2_LIMIT), (FAST, FAST_LIMIT))):
                 dF = np.sort(d[:n_set])
                 if dF.size >= 32 and dF[31] < limit:
                     first_tier += n_set == FAST2
@@ -226,3 +227,4 @@ def test_fast_set_model_matches_oracle(K):
     np.testing.assert_array_equal(got, nb["slot"])
     assert fallbacks < n // 4
     assert first_tier > n // 2
+
